@@ -1,0 +1,288 @@
+/*
+ * Elbow-routed MoE layer: plain CPU oracle (fp64).
+ *
+ * TEST INFRASTRUCTURE ONLY.  Only the test suite, the smoke check and the benchmark's
+ * CPU-baseline leg may load this library.  It shares no code, header, table or helper
+ * with the GPU library; the two meet only on the seeded input arrays.
+ *
+ * Everything is written as the paper defines it, in double precision, with plain loops:
+ *
+ *   routing (Section 2 "Elbow-Based Routing", Section 2.1 "Capped Expert Selection",
+ *            Appendix A.1 Algorithm 1 "Elbow Detection via Kneedle Approximation"):
+ *     p = softmax(l); sort p descending; p_min, p_max; normalise each sorted point to
+ *     the unit square; deviation D_i from the reference line; e = argmax D;
+ *     k = min(e + 1, K).
+ *   expert FFN: OLMoE's SwiGLU MLP, FFN(x) = W_down (silu(W_gate x) * (W_up x)).
+ *   layer:      y_t = [residual_t +] sum_{j<k_t} w_{t,j} FFN_{id_{t,j}}(x_t).
+ *
+ * Readings of the paper that this file fixes (the paper is silent or garbled there):
+ *   - orientation of the normalised curve: Algorithm 1 prints p'_i = (p_i - p_min)/(R+eps)
+ *     with p sorted descending, which makes D strictly decreasing and k = 1 for every
+ *     input.  The elbow-angle definition (Section 2.3) puts the first normalised point at
+ *     (0,0) and the last at (1,1), so the curve is flipped to increasing:
+ *     p'_i = (p_max - p_(i)) / (p_max - p_min + eps).  D_i is then the depth of sorted
+ *     point i below the chord joining the first and last sorted points.
+ *   - eps = 1e-8 by default (the paper does not give its value); a parameter here.
+ *   - argmax ties go to the smallest index (so a curve with no point below the chord
+ *     gives e = 0, k = 1).
+ *   - e in Algorithm 1 is 0-based and the algorithm returns e + 1; Section 2.1 caps that
+ *     count at K.
+ *   - the sort key is (logit descending, expert id ascending): softmax is strictly
+ *     increasing, so this is the descending order of p with ties broken by lower id.
+ *   - the weight of a selected expert is its full-softmax probability p, not
+ *     renormalised over the selected set (renorm = 1 renormalises instead).
+ *   - fixed top-K routing (the paper's baseline) is the same path with k = K.
+ *
+ * Parity pins for every function here live in tests/test_oracle_*.py (hand-worked
+ * curves, exact-rational brute force, invariants, the load-balance theorem, and special
+ * cases that reduce to library routines).
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+#define ORC_MODE_ELBOW 0
+#define ORC_MODE_TOPK 1
+
+int orc_version(void) { return 1; }
+
+/* Order indices by (key descending, index ascending): a plain insertion sort. */
+static void order_desc(const double *key, int N, int *sigma)
+{
+    for (int i = 0; i < N; ++i) sigma[i] = i;
+    for (int i = 1; i < N; ++i) {
+        int cur = sigma[i];
+        int j = i - 1;
+        while (j >= 0) {
+            int prev = sigma[j];
+            int before = key[prev] > key[cur] || (key[prev] == key[cur] && prev < cur);
+            if (before) break;
+            sigma[j + 1] = prev;
+            --j;
+        }
+        sigma[j + 1] = cur;
+    }
+}
+
+/*
+ * Steps after the sort (Algorithm 1, from p_min/p_max to the returned k, and the cap of
+ * Section 2.1), on one token's probabilities p[N] and its order sigma.
+ * Writes k, ids[0..K), w[0..K) (padding -1 / 0), and diagnostics:
+ *   e_out      argmax index (0-based, uncapped; -1 in top-K mode)
+ *   margin     D_{e} - max{D_i : min(i+1, K) != k}  (+inf when no such i, or top-K mode)
+ *   competitor the i attaining that max (-1 if none)
+ */
+static void select_experts(const double *p, const int *sigma, int N, int K, double eps,
+                           int mode, int renorm, int *k_out, int *ids, double *w,
+                           int *e_out, double *margin, int *competitor)
+{
+    int k;
+    int e = -1;
+    double mg = INFINITY;
+    int comp = -1;
+    if (mode == ORC_MODE_TOPK) {
+        k = K;
+    } else {
+        double D[N > 0 ? N : 1];
+        double p_max = p[sigma[0]];
+        double p_min = p[sigma[N - 1]];
+        double denom = p_max - p_min + eps;
+        for (int i = 0; i < N; ++i) {
+            double pn = (p_max - p[sigma[i]]) / denom;   /* normalised probability */
+            double xn = (double)i / (double)(N - 1);     /* normalised index */
+            D[i] = pn - xn;                              /* deviation from the line */
+        }
+        e = 0;
+        for (int i = 1; i < N; ++i)
+            if (D[i] > D[e]) e = i;                      /* first index wins ties */
+        k = e + 1 < K ? e + 1 : K;
+        for (int i = 0; i < N; ++i) {
+            int ki = i + 1 < K ? i + 1 : K;
+            if (ki == k) continue;
+            double gap = D[e] - D[i];
+            if (gap < mg) { mg = gap; comp = i; }
+        }
+    }
+    double sel = 0.0;
+    for (int j = 0; j < k; ++j) sel += p[sigma[j]];
+    for (int j = 0; j < K; ++j) {
+        if (j < k) {
+            ids[j] = sigma[j];
+            w[j] = renorm ? p[sigma[j]] / sel : p[sigma[j]];
+        } else {
+            ids[j] = -1;
+            w[j] = 0.0;
+        }
+    }
+    *k_out = k;
+    if (e_out) *e_out = e;
+    if (margin) *margin = mg;
+    if (competitor) *competitor = comp;
+}
+
+static int check_params(long T, int N, int K, double eps, int mode)
+{
+    if (T < 0 || N < 2 || K < 1 || K > N || !(eps >= 0.0)) return 1;
+    if (mode != ORC_MODE_ELBOW && mode != ORC_MODE_TOPK) return 1;
+    return 0;
+}
+
+/*
+ * Route T tokens from fp32 logits [T, N] (row-major).  Outputs k[T], ids[T, K], w[T, K];
+ * e, margin and competitor [T] are optional (NULL to skip).  Returns 0, or 1 on invalid
+ * arguments, 2 if a row has no finite logit.
+ */
+int orc_route(const float *logits, long T, int N, int K, double eps, int mode, int renorm,
+              int *k, int *ids, double *w, int *e, double *margin, int *competitor)
+{
+    if (check_params(T, N, K, eps, mode)) return 1;
+    int bad = 0;
+#pragma omp parallel for schedule(static) reduction(| : bad)
+    for (long t = 0; t < T; ++t) {
+        double l[N], p[N];
+        int sigma[N];
+        for (int j = 0; j < N; ++j) l[j] = (double)logits[t * N + j];
+        /* softmax (Section 2; Algorithm 1, first step) */
+        double mx = -INFINITY;
+        for (int j = 0; j < N; ++j) if (l[j] > mx) mx = l[j];
+        if (!isfinite(mx)) { bad = 1; continue; }
+        double s = 0.0;
+        for (int j = 0; j < N; ++j) { p[j] = exp(l[j] - mx); s += p[j]; }
+        for (int j = 0; j < N; ++j) p[j] /= s;
+        /* descending sort; ties (equal logits) by lower expert id */
+        order_desc(l, N, sigma);
+        select_experts(p, sigma, N, K, eps, mode, renorm, &k[t], ids + t * K, w + t * K,
+                       e ? &e[t] : NULL, margin ? &margin[t] : NULL,
+                       competitor ? &competitor[t] : NULL);
+    }
+    return bad ? 2 : 0;
+}
+
+/*
+ * Same selection on given probability vectors p[T, N] (no softmax): the sort key is p
+ * itself, ties by lower id.  Used to pin the selection rule on exact curves.
+ */
+int orc_route_from_probs(const double *p, long T, int N, int K, double eps, int mode,
+                         int renorm, int *k, int *ids, double *w, int *e, double *margin,
+                         int *competitor)
+{
+    if (check_params(T, N, K, eps, mode)) return 1;
+    for (long t = 0; t < T; ++t) {
+        int sigma[N];
+        order_desc(p + t * N, N, sigma);
+        select_experts(p + t * N, sigma, N, K, eps, mode, renorm, &k[t], ids + t * K,
+                       w + t * K, e ? &e[t] : NULL, margin ? &margin[t] : NULL,
+                       competitor ? &competitor[t] : NULL);
+    }
+    return 0;
+}
+
+/* Router logits of one token, l = W_r x (the router is a bias-free linear layer). */
+static void logits_one(const float *x, const float *Wr, int d, int N, double *out)
+{
+    for (int n = 0; n < N; ++n) {
+        double acc = 0.0;
+        for (int c = 0; c < d; ++c) acc += (double)Wr[(long)n * d + c] * (double)x[c];
+        out[n] = acc;
+    }
+}
+
+/* Router logits for T tokens: out[T, N] (fp64). */
+void orc_router_logits(const float *x, const float *Wr, long T, int d, int N, double *out)
+{
+#pragma omp parallel for schedule(static)
+    for (long t = 0; t < T; ++t) logits_one(x + t * d, Wr, d, N, out + t * N);
+}
+
+static double silu(double z) { return z / (1.0 + exp(-z)); }
+
+/*
+ * One expert's SwiGLU MLP on one token: out[d] = W_down (silu(W_gate x) * (W_up x)).
+ * Wgu is that expert's [2m, d] block (gate rows first), Wd its [d, m] block.
+ */
+static void expert_ffn(const float *x, const float *Wgu, const float *Wd, int d, int m,
+                       double *h, double *out)
+{
+    for (int i = 0; i < m; ++i) {
+        double g = 0.0, u = 0.0;
+        const float *wg = Wgu + (long)i * d;
+        const float *wu = Wgu + (long)(m + i) * d;
+        for (int c = 0; c < d; ++c) {
+            g += (double)wg[c] * (double)x[c];
+            u += (double)wu[c] * (double)x[c];
+        }
+        h[i] = silu(g) * u;
+    }
+    for (int r = 0; r < d; ++r) {
+        double acc = 0.0;
+        const float *wd = Wd + (long)r * m;
+        for (int i = 0; i < m; ++i) acc += (double)wd[i] * h[i];
+        out[r] = acc;
+    }
+}
+
+/*
+ * Expert part of the layer for a list of tokens, given their routing:
+ *   y[r] = [residual[tok_r] +] sum_{j<k[r]} w[r, j] * FFN_{ids[r, j]}(x[tok_r])
+ * tok[n_tok] indexes rows of x [T, d]; k/ids/w are per listed token ([n_tok], [n_tok, K]).
+ * Accumulation over j is in rank order, in double.  Returns 0 or 1 on a bad expert id.
+ */
+int orc_moe_experts(const float *x, const float *Wgu, const float *Wd, const float *residual,
+                    long T, int d, int N, int m, int K, const long *tok, long n_tok,
+                    const int *k, const int *ids, const double *w, double *y)
+{
+    int bad = 0;
+#pragma omp parallel for schedule(dynamic, 1) reduction(| : bad)
+    for (long r = 0; r < n_tok; ++r) {
+        long t = tok[r];
+        if (t < 0 || t >= T) { bad = 1; continue; }
+        double *h = (double *)malloc(sizeof(double) * (size_t)m);
+        double *o = (double *)malloc(sizeof(double) * (size_t)d);
+        double *acc = y + r * d;
+        for (int c = 0; c < d; ++c) acc[c] = residual ? (double)residual[t * d + c] : 0.0;
+        for (int j = 0; j < k[r]; ++j) {
+            int ex = ids[r * K + j];
+            if (ex < 0 || ex >= N) { bad = 1; break; }
+            expert_ffn(x + t * d, Wgu + (long)ex * 2 * m * d, Wd + (long)ex * d * m, d, m, h, o);
+            for (int c = 0; c < d; ++c) acc[c] += w[r * K + j] * o[c];
+        }
+        free(h);
+        free(o);
+    }
+    return bad;
+}
+
+/*
+ * Whole layer for a list of tokens: router logits (fp64), routing on those logits,
+ * then the expert part.  Routing outputs and the fp64 logits are returned for the
+ * listed tokens.  Returns 0, 1 on invalid arguments, 2 on a row with no finite logit.
+ */
+int orc_moe_forward(const float *x, const float *Wr, const float *Wgu, const float *Wd,
+                    const float *residual, long T, int d, int N, int m, int K, double eps,
+                    int mode, int renorm, const long *tok, long n_tok, double *y,
+                    double *logits, int *k, int *ids, double *w, double *margin)
+{
+    if (check_params(T, N, K, eps, mode) || d < 1 || m < 1) return 1;
+    for (long r = 0; r < n_tok; ++r)
+        if (tok[r] < 0 || tok[r] >= T) return 1;
+    int bad = 0;
+#pragma omp parallel for schedule(static) reduction(| : bad)
+    for (long r = 0; r < n_tok; ++r) {
+        long t = tok[r];
+        logits_one(x + t * d, Wr, d, N, logits + r * N);
+        double l[N], p[N];
+        int sigma[N];
+        double mx = -INFINITY;
+        for (int j = 0; j < N; ++j) { l[j] = logits[r * N + j]; if (l[j] > mx) mx = l[j]; }
+        if (!isfinite(mx)) { bad = 1; continue; }
+        double s = 0.0;
+        for (int j = 0; j < N; ++j) { p[j] = exp(l[j] - mx); s += p[j]; }
+        for (int j = 0; j < N; ++j) p[j] /= s;
+        order_desc(l, N, sigma);
+        select_experts(p, sigma, N, K, eps, mode, renorm, &k[r], ids + r * K, w + r * K,
+                       NULL, margin ? &margin[r] : NULL, NULL);
+    }
+    if (bad) return 2;
+    return orc_moe_experts(x, Wgu, Wd, residual, T, d, N, m, K, tok, n_tok, k, ids, w, y);
+}
