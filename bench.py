@@ -1,0 +1,218 @@
+"""Benchmark: elbow-routed MoE layer on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload olmoe-prefill]
+
+One step = one whole layer (router GEMM, routing, dispatch, grouped SwiGLU expert GEMMs,
+combine) over one batch of synthetic OLMoE-shaped tokens already resident in HBM.
+Prints ONE JSON line with tokens/s, the roofline of the dominant kernel (the grouped
+gate/up expert GEMM on MFMA), the fixed top-8 baseline through the same kernels, the
+routing kernel's HBM fraction on the routing-only workload, and the fp64 CPU oracle timed
+on a bounded token sample on this host.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0         # MI355X HBM3E
+
+WORKLOADS = {
+    # name: (T, d, N, m, K)
+    "olmoe-prefill": (4096, 2048, 64, 1024, 8),
+    "olmoe-decode": (64, 2048, 64, 1024, 8),
+}
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def sha1(path):
+    return hashlib.sha1(open(path, "rb").read()).hexdigest()[:12]
+
+
+def time_layer(B, torch, args_gpu, K, mode, steps, warmup, profile):
+    x, Wr, Wgu, Wd = args_gpu
+    out = torch.empty_like(x)
+    for _ in range(warmup):
+        B.elb_moe_forward(x, Wr, Wgu, Wd, K=K, mode=mode, out=out)
+    torch.cuda.synchronize()
+    B.elb_profile_read()
+    B.elb_profile_enable(profile)
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        B.elb_moe_forward(x, Wr, Wgu, Wd, K=K, mode=mode, out=out)
+    torch.cuda.synchronize()
+    dt = time.perf_counter() - t0
+    B.elb_profile_enable(False)
+    kern = B.elb_profile_read() if profile else {}
+    return dt / steps * 1e3, {n: ms / cnt for n, (ms, cnt) in kern.items()}
+
+
+def routing_only(B, torch, T=65536, N=64, K=8, nbuf=32, iters=64):
+    """Routing kernel alone on the routing-only workload (planted logits), rotating over
+    nbuf distinct logit buffers (nbuf * 16.8 MB > the 256 MB last-level cache)."""
+    from paper_2608_04401_amd import synth
+    lg = torch.from_numpy(synth.planted_logits(T, N, seed=0)).cuda()
+    bufs = [lg.clone() for _ in range(nbuf)]
+    k = torch.empty(T, dtype=torch.int32, device="cuda")
+    ids = torch.empty((T, K), dtype=torch.int32, device="cuda")
+    w = torch.empty((T, K), dtype=torch.float32, device="cuda")
+    import ctypes as C
+    L = B.lib()
+    p = B.RouteParams(K, 1e-8, B.MODE_ELBOW, 0)
+    st = C.c_void_p(torch.cuda.current_stream().cuda_stream)
+    for i in range(8):
+        L.elb_route(C.c_void_p(bufs[i].data_ptr()), T, N, C.byref(p), C.c_void_p(k.data_ptr()),
+                    C.c_void_p(ids.data_ptr()), C.c_void_p(w.data_ptr()), st)
+    torch.cuda.synchronize()
+    B.elb_profile_read()
+    B.elb_profile_enable(True)
+    for i in range(iters):
+        L.elb_route(C.c_void_p(bufs[i % nbuf].data_ptr()), T, N, C.byref(p),
+                    C.c_void_p(k.data_ptr()), C.c_void_p(ids.data_ptr()),
+                    C.c_void_p(w.data_ptr()), st)
+    torch.cuda.synchronize()
+    B.elb_profile_enable(False)
+    ms, cnt = B.elb_profile_read()["route"]
+    us = ms / cnt * 1e3
+    nbytes = T * N * 4 + T * (4 + 4 * K + 4 * K)
+    gbs = nbytes / (us * 1e-6) / 1e9
+    return {"workload": "routing-only T=%d N=%d K=%d planted logits" % (T, N, K),
+            "kernel": "route", "us": round(us, 3), "bytes": nbytes, "GB/s": round(gbs, 1),
+            "peak": PEAK_HBM_GBS, "frac": round(gbs / PEAK_HBM_GBS, 4)}
+
+
+def cpu_baseline(L, K, target_s=12.0):
+    """The fp64 oracle on a bounded token sample of the same workload, on this host."""
+    from oracle import oracle as O
+    O.build()
+    threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+    rng = np.random.default_rng(123)
+    n = 16
+    while True:
+        tok = np.sort(rng.choice(L.T, n, replace=False))
+        t0 = time.perf_counter()
+        O.moe_forward(L.x, L.W_router, L.W_gu, L.W_down, K=K, tokens=tok)
+        dt = time.perf_counter() - t0
+        if dt >= target_s or n >= L.T:
+            break
+        n = min(L.T, max(n * 2, int(n * target_s / max(dt, 1e-3) * 1.1)))
+    return {"value": round(n / dt, 2), "unit": "tokens/s", "cores": threads, "kind": "oracle",
+            "sample": "%d of %d tokens of the same layer (fp64 router, routing and experts), "
+                      "%.1f s" % (n, L.T, dt)}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default="olmoe-prefill", choices=sorted(WORKLOADS))
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-routing", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(--gpus %d requested)" % args.gpus, file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2608_04401_amd import binding as B
+    from paper_2608_04401_amd import synth
+
+    if not torch.cuda.is_available():
+        print("no GPU visible", file=sys.stderr)
+        sys.exit(1)
+    B.lib()
+    T, d, N, m, K = WORKLOADS[args.workload]
+    log("generating %s inputs T=%d d=%d N=%d m=%d" % (args.workload, T, d, N, m))
+    L = synth.moe_layer(T, d, N, m, dtype="bf16", seed=0)
+    gpu = tuple(torch.from_numpy(a).to("cuda").to(torch.bfloat16)
+                for a in (L.x, L.W_router, L.W_gu, L.W_down))
+
+    # routing statistics of this batch (for the useful-FLOP count)
+    _, dbg = B.elb_moe_forward(*gpu, K=K, debug=True)
+    _, dbg_top = B.elb_moe_forward(*gpu, K=K, mode=B.MODE_TOPK, debug=True)
+    torch.cuda.synchronize()
+    sum_k = int(dbg["k"].sum().item())
+    sum_k_top = int(dbg_top["k"].sum().item())
+    counts = dbg["counts"].cpu().numpy()
+    counts_top = dbg_top["counts"].cpu().numpy()
+
+    log("timing elbow layer: %d warmup, %d steps" % (args.warmup, args.steps))
+    ms, kern = time_layer(B, torch, gpu, K, B.MODE_ELBOW, args.steps, args.warmup, True)
+    log("timing top-8 baseline")
+    ms_top, kern_top = time_layer(B, torch, gpu, K, B.MODE_TOPK, args.steps, args.warmup, True)
+    # same timed loop without the per-kernel events, for the event overhead
+    ms_noev, _ = time_layer(B, torch, gpu, K, B.MODE_ELBOW, args.steps, 2, False)
+
+    g1 = "gemm_gate_up_bf16"
+    flop_g1 = 4.0 * d * m * sum_k            # useful FLOPs of the gate/up GEMM per launch
+    us_g1 = kern[g1] * 1e3
+    achieved = flop_g1 / (us_g1 * 1e-6) / 1e12
+    traffic = None
+    tfile = os.path.join(ROOT, "profiles", "gemm_gate_up_bf16_olmoe_prefill_traffic.json")
+    if os.path.exists(tfile):
+        tj = json.load(open(tfile))
+        if tj.get("source_sha1") == sha1(os.path.join(ROOT, "paper_2608_04401_amd", "csrc",
+                                                      "gemm.hip")):
+            traffic = tj.get("bytes_per_launch")
+    flop_all = 6.0 * d * m * sum_k
+    res = {
+        "metric": "elbow-routed MoE layer tokens/s (OLMoE shape)",
+        "value": round(T / (ms * 1e-3), 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": "%s: T=%d d_model=%d N=%d experts, SwiGLU intermediate %d, "
+                               "elbow routing capped at K=%d, bf16 weights N(0,0.02), bf16 "
+                               "x N(0,1), seed 0" % (args.workload, T, d, N, m, K),
+                   "global_batch": T, "K": K},
+        "roofline": {"bound": "mfma", "kernel": g1, "achieved": round(achieved, 1),
+                     "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                     "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": traffic,
+                     "flop_per_launch": flop_g1, "us_per_launch": round(us_g1, 2)},
+        "mean_k": round(sum_k / T, 4),
+        "expert_flop_fraction_of_peak": round(flop_all / (sum(
+            kern[n] for n in kern if n.startswith("gemm")) * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+        "kernels_us": {n: round(v * 1e3, 2) for n, v in kern.items()},
+        "ms_per_step_without_kernel_events": round(ms_noev, 4),
+        "topk_baseline": {"value": round(T / (ms_top * 1e-3), 1), "unit": "tokens/s",
+                          "ms_per_step": round(ms_top, 4), "sum_k": sum_k_top,
+                          "kernels_us": {n: round(v * 1e3, 2) for n, v in kern_top.items()}},
+        "elbow_vs_topk_latency_change_pct": round((ms - ms_top) / ms_top * 100, 2),
+        "paper_context": "the paper reports a 5.3% average latency reduction on OLMoE on one "
+                         "NVIDIA H200 (context only)",
+    }
+    from paper_2608_04401_amd import stats
+    res["load_balance"] = {k2: (round(v, 5) if isinstance(v, float) else v) for k2, v in
+                           stats.load_balance_report(counts, counts_top, K, T).items()}
+    if not args.no_routing:
+        log("routing-only kernel")
+        res["routing_kernel"] = routing_only(B, torch)
+    if not args.no_cpu_baseline:
+        log("cpu baseline (oracle)")
+        res["cpu_baseline"] = cpu_baseline(L, K)
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

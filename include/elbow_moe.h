@@ -1,0 +1,172 @@
+/*
+ * elbow_moe.h - C ABI of the elbow-routed MoE layer for AMD MI355X (gfx950).
+ *
+ * The layer (Section 2 of "Elbow-based MoE Routing: A Training-Free Inference Time Plugin
+ * for Expert Selection"): for each token, router logits l = W_r x, probabilities
+ * p = softmax(l), the probabilities sorted in descending order, a Kneedle-style elbow
+ * index e on that sorted curve (Appendix A.1, Algorithm 1), the expert count
+ * k = min(e + 1, K) capped at the model's top-K (Section 2.1), and the output
+ * y = sum_{j<k} w_j FFN_{id_j}(x) over the selected experts, FFN being a bias-free SwiGLU
+ * MLP.  Fixed top-K routing (the paper's baseline) runs through the same path.
+ *
+ * Conventions for every entry point:
+ *  - All tensor pointers are DEVICE pointers owned by the caller; row-major, densely packed.
+ *    The library never allocates, frees or synchronises device memory; scratch space
+ *    comes only from the caller's workspace.  Nothing is retained between calls.
+ *  - `stream` is a hipStream_t passed as void* (NULL = the null stream).  Kernels are
+ *    enqueued on it and the call returns without waiting for them.
+ *  - Arguments are validated on the host BEFORE anything is enqueued.  On any error
+ *    nothing is launched and nothing is written.  T = 0 is valid and enqueues nothing.
+ *  - Return value: ELB_OK (0) or one of the ELB_ERR_* codes below; elb_last_error()
+ *    gives a message for the last failing call of the calling thread.
+ *  - Calls on the same stream are ordered; concurrent calls on different streams must not
+ *    share output or workspace buffers.
+ *  - Inputs must be finite, except that -inf logits are allowed when each row has at
+ *    least one finite logit.  NaN inputs give unspecified (but in-bounds) results.
+ *
+ * Data types: ELB_F32 tensors are float; ELB_BF16 tensors are bfloat16 (uint16 storage,
+ * round-to-nearest-even).  Router logits, routing weights and all accumulation are fp32.
+ */
+#ifndef ELBOW_MOE_H
+#define ELBOW_MOE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define ELB_ABI_VERSION 1
+
+/* Largest supported expert count N and cap K. */
+#define ELB_MAX_EXPERTS 64
+#define ELB_MAX_K 16
+
+typedef enum {
+    ELB_OK = 0,
+    ELB_ERR_INVALID_ARG = 1, /* null pointer, negative size, K outside [1, N], eps < 0, ... */
+    ELB_ERR_UNSUPPORTED = 2, /* a size outside what the kernels implement (e.g. N > 64) */
+    ELB_ERR_WORKSPACE = 3,   /* workspace missing or smaller than elb_*_workspace_bytes */
+    ELB_ERR_HIP = 4          /* a HIP launch error (hipGetLastError after the launch) */
+} elb_status;
+
+typedef enum { ELB_F32 = 0, ELB_BF16 = 1 } elb_dtype;
+
+typedef enum {
+    ELB_MODE_ELBOW = 0, /* k = min(e + 1, K), Algorithm 1 with the cap of Section 2.1 */
+    ELB_MODE_TOPK = 1   /* k = K: the fixed top-K routing the method prunes */
+} elb_mode;
+
+typedef struct {
+    int32_t K;           /* cap: the model's top-K (8 for OLMoE); 1 <= K <= min(N, ELB_MAX_K) */
+    float eps;           /* the normaliser's epsilon of Algorithm 1 (default 1e-8); >= 0 */
+    int32_t mode;        /* elb_mode */
+    int32_t renormalize; /* 0: w_j = p_(j) (full-softmax probability); 1: w_j = p_(j) /
+                            sum_{i<k} p_(i) */
+} elb_route_params;
+
+/* ABI version (ELB_ABI_VERSION of the built library). */
+int elb_abi_version(void);
+
+/* Static description of a status code. */
+const char *elb_status_str(int status);
+
+/* Message of the last failing call on the calling thread ("" if none). */
+const char *elb_last_error(void);
+
+/*
+ * Router logits (Section 2: a learned router produces logits l(x) in R^N per token).
+ *   x        [T, d]  dtype            token activations
+ *   W_router [N, d]  dtype            router weight (nn.Linear layout, no bias)
+ *   logits   [T, N]  float (output)   l = x W_router^T, fp32 accumulation
+ * Requirements: 2 <= N <= ELB_MAX_EXPERTS, d >= 1 (d % 32 == 0 for ELB_BF16).
+ */
+int elb_router_logits(const void *x, const void *W_router, int64_t T, int32_t d, int32_t N,
+                      int32_t dtype, float *logits, void *stream);
+
+/*
+ * Routing (Section 2 and 2.1; Appendix A.1 Algorithm 1).  Per token:
+ *   p = softmax(l); sort p descending (equal logits: lower expert id first);
+ *   p'_i = (p_(0) - p_(i)) / (p_(0) - p_(N-1) + eps),  x'_i = i / (N - 1),
+ *   D_i = p'_i - x'_i,  e = smallest index maximising D,  k = min(e + 1, K)
+ *   (ELB_MODE_TOPK: k = K).
+ * The normalised curve runs from (0,0) to (1,1), the orientation of the paper's elbow
+ * angle (Section 2.3); D_i is the depth of sorted point i below the chord.
+ *   logits [T, N] float   input
+ *   k      [T]    int32   output, 1 <= k <= K
+ *   ids    [T, K] int32   output, expert ids in descending-probability order; -1 for j >= k
+ *   w      [T, K] float   output, weights (see elb_route_params.renormalize); 0 for j >= k
+ * Requirements: 2 <= N <= ELB_MAX_EXPERTS; params valid.
+ */
+int elb_route(const float *logits, int64_t T, int32_t N, const elb_route_params *params,
+              int32_t *k, int32_t *ids, float *w, void *stream);
+
+/*
+ * Variable-k dispatch: expert-major token lists built from a routing (deterministic:
+ * within an expert, rows are in increasing token order).
+ *   k, ids            [T], [T, K]   a routing as written by elb_route
+ *   counts    [N]     int32 output  assignments per expert, sum = sum_t k_t
+ *   offsets   [N + 1] int32 output  exclusive prefix sum of counts (offsets[N] = sum k)
+ *   row_token [T * K] int32 output  row r of the expert-major order holds token
+ *                                   row_token[r]; rows >= offsets[N] are left untouched
+ *   inv       [T, K]  int32 output  row of (t, j) for j < k_t, -1 otherwise
+ *   workspace          device scratch of at least elb_dispatch_workspace_bytes(T, N) bytes
+ */
+size_t elb_dispatch_workspace_bytes(int64_t T, int32_t N);
+int elb_dispatch(const int32_t *k, const int32_t *ids, int64_t T, int32_t N, int32_t K,
+                 int32_t *counts, int32_t *offsets, int32_t *row_token, int32_t *inv,
+                 void *workspace, size_t workspace_bytes, void *stream);
+
+/*
+ * Expert part of the layer for a given routing: dispatch, the grouped SwiGLU expert
+ * GEMMs and the weighted combine, in rank order with fp32 accumulation:
+ *   y_t = [residual_t +] sum_{j<k_t} w_tj FFN_{ids_tj}(x_t),
+ *   FFN_e(x) = W_down[e] (silu(W_gate[e] x) * (W_up[e] x)),  silu(z) = z / (1 + e^-z).
+ *   x         [T, d]      dtype
+ *   W_gate_up [N, 2m, d]  dtype   rows [0, m) = W_gate[e], rows [m, 2m) = W_up[e]
+ *   W_down    [N, d, m]   dtype
+ *   k, ids, w             a routing ([T], [T, K], [T, K]) as written by elb_route
+ *   residual  [T, d]      dtype   optional (NULL: none)
+ *   y         [T, d]      dtype   output; may alias residual, must not alias x
+ *   workspace             at least elb_moe_workspace_bytes(T, d, N, m, K, dtype) bytes
+ * Requirements: 2 <= N <= ELB_MAX_EXPERTS; 1 <= K <= min(N, ELB_MAX_K);
+ * ELB_BF16: d % 64 == 0 and m % 64 == 0; ELB_F32: d % 4 == 0 and m % 4 == 0.
+ */
+size_t elb_moe_workspace_bytes(int64_t T, int32_t d, int32_t N, int32_t m, int32_t K,
+                               int32_t dtype);
+int elb_moe_experts(const void *x, const void *W_gate_up, const void *W_down,
+                    const int32_t *k, const int32_t *ids, const float *w, const void *residual,
+                    int64_t T, int32_t d, int32_t N, int32_t m, int32_t K, int32_t dtype,
+                    void *y, void *workspace, size_t workspace_bytes, void *stream);
+
+/*
+ * The whole layer: elb_router_logits, elb_route, then elb_moe_experts, on one stream,
+ * with no host round trip.  Arguments as above; the optional debug outputs (NULL to
+ * skip) receive the intermediate results of this call:
+ *   logits_out [T, N] float, k_out [T], ids_out [T, K], w_out [T, K],
+ *   counts_out [N] int32 (assignments per expert).
+ */
+int elb_moe_forward(const void *x, const void *W_router, const void *W_gate_up,
+                    const void *W_down, const void *residual, int64_t T, int32_t d, int32_t N,
+                    int32_t m, int32_t dtype, const elb_route_params *params, void *y,
+                    void *workspace, size_t workspace_bytes, float *logits_out,
+                    int32_t *k_out, int32_t *ids_out, float *w_out, int32_t *counts_out,
+                    void *stream);
+
+/*
+ * Per-kernel timing (host-side hipEvents around each launch the library makes).
+ * elb_profile_enable(1) starts recording on the calling process; every launch then
+ * records a start/stop event pair on its stream.  elb_profile_read() synchronises on the
+ * recorded events, fills up to `cap` entries of names (static strings), total
+ * milliseconds and launch counts per kernel, clears the records and returns the number
+ * of kernels (or a negative elb_status).  Not for use under graph capture.
+ */
+int elb_profile_enable(int on);
+int elb_profile_read(const char **names, double *total_ms, int64_t *launches, int cap);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* ELBOW_MOE_H */

@@ -286,3 +286,39 @@ int orc_moe_forward(const float *x, const float *Wr, const float *Wgu, const flo
     if (bad) return 2;
     return orc_moe_experts(x, Wgu, Wd, residual, T, d, N, m, K, tok, n_tok, k, ids, w, y);
 }
+
+/*
+ * Dispatch view of a routing: the expert-major token lists that a variable-k layer runs its
+ * expert MLPs over (each token t appears once in the list of each of its k_t experts).
+ *   counts[e]     = #{(t, j < k_t) : ids[t, j] = e}; their sum is sum_t k_t
+ *   offsets[e]    = counts[0] + ... + counts[e-1]  (offsets[N] = sum_t k_t)
+ *   row_token[r]  = the token of row r; rows of expert e are its tokens in increasing order
+ *   inv[t, j]     = the row of (t, j) for j < k_t, -1 otherwise
+ * Returns 0, or 1 if an id outside [0, N) is selected.
+ */
+int orc_dispatch(const int *k, const int *ids, long T, int N, int K, int *counts, int *offsets,
+                 int *row_token, int *inv)
+{
+    for (int e = 0; e < N; ++e) counts[e] = 0;
+    for (long t = 0; t < T; ++t)
+        for (int j = 0; j < K; ++j) {
+            inv[t * K + j] = -1;
+            if (j >= k[t]) continue;
+            int e = ids[t * K + j];
+            if (e < 0 || e >= N) return 1;
+            counts[e] += 1;
+        }
+    offsets[0] = 0;
+    for (int e = 0; e < N; ++e) offsets[e + 1] = offsets[e] + counts[e];
+    for (int e = 0; e < N; ++e) {
+        int r = offsets[e];
+        for (long t = 0; t < T; ++t)          /* tokens in increasing order */
+            for (int j = 0; j < k[t] && j < K; ++j)
+                if (ids[t * K + j] == e) {
+                    row_token[r] = (int)t;
+                    inv[t * K + j] = r;
+                    ++r;
+                }
+    }
+    return 0;
+}

@@ -76,8 +76,25 @@ class OracleLib:
         lib.orc_moe_forward.argtypes = [P, P, P, P, P, C.c_long, C.c_int, C.c_int, C.c_int,
                                         C.c_int, C.c_double, C.c_int, C.c_int, P, C.c_long,
                                         P, P, P, P, P, P]
+        lib.orc_dispatch.argtypes = [P, P, C.c_long, C.c_int, C.c_int, P, P, P, P]
         self.lib = lib
         self.path = path
+
+    def dispatch(self, k, ids, N: int):
+        """Expert-major lists of a routing -> (counts [N], offsets [N+1], row_token [sum k],
+        inv [T, K]) as int32."""
+        kk = np.ascontiguousarray(k, np.int32)
+        ii = np.ascontiguousarray(ids, np.int32)
+        T, K = ii.shape
+        counts = np.empty(N, np.int32)
+        offsets = np.empty(N + 1, np.int32)
+        row_token = np.empty(int(np.minimum(kk, K).clip(0).sum()), np.int32)
+        inv = np.empty((T, K), np.int32)
+        rc = self.lib.orc_dispatch(_ptr(kk), _ptr(ii), T, N, K, _ptr(counts), _ptr(offsets),
+                                   _ptr(row_token), _ptr(inv))
+        if rc != 0:
+            raise ValueError("oracle dispatch: expert id out of range")
+        return counts, offsets, row_token, inv
 
     def _route(self, fn, arr, N, K, eps, mode, renorm):
         T = arr.shape[0]
@@ -188,6 +205,10 @@ def router_logits(*a, **kw) -> np.ndarray:
 
 def moe_experts(*a, **kw) -> np.ndarray:
     return _lib().moe_experts(*a, **kw)
+
+
+def dispatch(*a, **kw):
+    return _lib().dispatch(*a, **kw)
 
 
 def moe_forward(*a, **kw) -> LayerResult:

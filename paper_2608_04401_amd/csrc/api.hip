@@ -1,0 +1,364 @@
+// C ABI of libelbow_moe: argument validation, workspace carving, launch order, timing hooks.
+#include <algorithm>
+#include <atomic>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <map>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "common.h"
+
+namespace elb {
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const char* fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof(buf), fmt, ap);
+    va_end(ap);
+    g_err = buf;
+    return code;
+}
+
+int hip_status(hipError_t e, const char* where) {
+    if (e == hipSuccess) return ELB_OK;
+    return fail(ELB_ERR_HIP, "%s: %s", where, hipGetErrorString(e));
+}
+
+constexpr size_t kAlign = 256;
+inline size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
+
+// Sub-buffers carved from the caller's workspace, in this order.
+struct Layout {
+    size_t hist, tile_off, counts, offsets, row_token, inv, H, Y;  // expert part
+    size_t logits, k, ids, w;                                      // routing (forward only)
+    size_t experts_end, total;
+};
+
+size_t esize(int dtype) { return dtype == ELB_BF16 ? 2 : 4; }
+
+Layout layout(int64_t T, int d, int N, int m, int K, int dtype) {
+    Layout L{};
+    size_t o = 0;
+    auto take = [&](size_t bytes) {
+        const size_t at = o;
+        o += align_up(bytes);
+        return at;
+    };
+    const size_t rows = (size_t)T * K;
+    L.hist = take((size_t)dispatch_groups(T) * N * 4);
+    L.tile_off = take((size_t)(N + 1) * 4);
+    L.counts = take((size_t)N * 4);
+    L.offsets = take((size_t)(N + 1) * 4);
+    L.row_token = take(rows * 4);
+    L.inv = take(rows * 4);
+    L.H = take(rows * m * esize(dtype));
+    L.Y = take(rows * d * esize(dtype));
+    L.experts_end = o;
+    L.logits = take((size_t)T * N * 4);
+    L.k = take((size_t)T * 4);
+    L.ids = take(rows * 4);
+    L.w = take(rows * 4);
+    L.total = o;
+    return L;
+}
+
+int64_t max_tiles(int64_t T, int K, int N, int tile_rows) {
+    // sum_e ceil(c_e / BM) <= (sum_e c_e + N (BM - 1)) / BM, sum_e c_e <= T K
+    return (T * K + (int64_t)N * (tile_rows - 1)) / tile_rows;
+}
+
+int check_route_params(int N, const elb_route_params* p) {
+    if (!p) return fail(ELB_ERR_INVALID_ARG, "params is NULL");
+    if (N < 2) return fail(ELB_ERR_INVALID_ARG, "N = %d: need at least 2 experts", N);
+    if (N > ELB_MAX_EXPERTS)
+        return fail(ELB_ERR_UNSUPPORTED, "N = %d exceeds ELB_MAX_EXPERTS = %d", N,
+                    ELB_MAX_EXPERTS);
+    if (p->K < 1 || p->K > N)
+        return fail(ELB_ERR_INVALID_ARG, "K = %d outside [1, N = %d]", p->K, N);
+    if (p->K > ELB_MAX_K)
+        return fail(ELB_ERR_UNSUPPORTED, "K = %d exceeds ELB_MAX_K = %d", p->K, ELB_MAX_K);
+    if (!(p->eps >= 0.f) || !std::isfinite(p->eps))
+        return fail(ELB_ERR_INVALID_ARG, "eps = %g must be finite and >= 0", (double)p->eps);
+    if (p->mode != ELB_MODE_ELBOW && p->mode != ELB_MODE_TOPK)
+        return fail(ELB_ERR_INVALID_ARG, "mode = %d is not an elb_mode", p->mode);
+    if (p->renormalize != 0 && p->renormalize != 1)
+        return fail(ELB_ERR_INVALID_ARG, "renormalize = %d must be 0 or 1", p->renormalize);
+    return ELB_OK;
+}
+
+int check_dtype(int dtype) {
+    if (dtype != ELB_F32 && dtype != ELB_BF16)
+        return fail(ELB_ERR_INVALID_ARG, "dtype = %d is not an elb_dtype", dtype);
+    return ELB_OK;
+}
+
+int check_expert_dims(int64_t T, int d, int N, int m, int K, int dtype) {
+    if (int rc = check_dtype(dtype)) return rc;
+    if (T < 0) return fail(ELB_ERR_INVALID_ARG, "T = %lld < 0", (long long)T);
+    if (N < 2) return fail(ELB_ERR_INVALID_ARG, "N = %d: need at least 2 experts", N);
+    if (N > ELB_MAX_EXPERTS)
+        return fail(ELB_ERR_UNSUPPORTED, "N = %d exceeds ELB_MAX_EXPERTS = %d", N,
+                    ELB_MAX_EXPERTS);
+    if (K < 1 || K > N) return fail(ELB_ERR_INVALID_ARG, "K = %d outside [1, N = %d]", K, N);
+    if (K > ELB_MAX_K)
+        return fail(ELB_ERR_UNSUPPORTED, "K = %d exceeds ELB_MAX_K = %d", K, ELB_MAX_K);
+    if (d < 1 || m < 1) return fail(ELB_ERR_INVALID_ARG, "d = %d, m = %d must be >= 1", d, m);
+    const int g = dtype == ELB_BF16 ? 64 : 16;
+    if (d % g || m % g)
+        return fail(ELB_ERR_INVALID_ARG, "d = %d and m = %d must be multiples of %d for %s", d,
+                    m, g, dtype == ELB_BF16 ? "bf16" : "f32");
+    if (T * (int64_t)K >= (int64_t)1 << 31)
+        return fail(ELB_ERR_UNSUPPORTED, "T * K = %lld assignments exceed 2^31",
+                    (long long)(T * K));
+    return ELB_OK;
+}
+
+// ---- per-kernel timing ----
+struct Rec {
+    const char* name;
+    hipEvent_t a, b;
+};
+std::atomic<bool> g_prof_on{false};
+std::mutex g_prof_mu;
+std::vector<Rec> g_recs;
+std::vector<hipEvent_t> g_pool;
+
+hipEvent_t pool_get() {
+    if (!g_pool.empty()) {
+        hipEvent_t e = g_pool.back();
+        g_pool.pop_back();
+        return e;
+    }
+    hipEvent_t e = nullptr;
+    if (hipEventCreate(&e) != hipSuccess) return nullptr;
+    return e;
+}
+
+}  // namespace
+
+ProfileScope::ProfileScope(const char* name, hipStream_t s) : name_(name), s_(s), slot_(-1) {
+    if (!g_prof_on.load(std::memory_order_relaxed)) return;
+    std::lock_guard<std::mutex> lk(g_prof_mu);
+    Rec r{name, pool_get(), pool_get()};
+    if (!r.a || !r.b) return;
+    (void)hipEventRecord(r.a, s);
+    g_recs.push_back(r);
+    slot_ = (int)g_recs.size() - 1;
+}
+
+ProfileScope::~ProfileScope() {
+    if (slot_ < 0) return;
+    std::lock_guard<std::mutex> lk(g_prof_mu);
+    if (slot_ < (int)g_recs.size()) (void)hipEventRecord(g_recs[slot_].b, s_);
+}
+
+}  // namespace elb
+
+using namespace elb;
+
+extern "C" {
+
+int elb_abi_version(void) { return ELB_ABI_VERSION; }
+
+const char* elb_status_str(int status) {
+    switch (status) {
+        case ELB_OK: return "ELB_OK";
+        case ELB_ERR_INVALID_ARG: return "ELB_ERR_INVALID_ARG";
+        case ELB_ERR_UNSUPPORTED: return "ELB_ERR_UNSUPPORTED";
+        case ELB_ERR_WORKSPACE: return "ELB_ERR_WORKSPACE";
+        case ELB_ERR_HIP: return "ELB_ERR_HIP";
+        default: return "ELB_ERR_UNKNOWN";
+    }
+}
+
+const char* elb_last_error(void) { return g_err.c_str(); }
+
+int elb_router_logits(const void* x, const void* W_router, int64_t T, int32_t d, int32_t N,
+                      int32_t dtype, float* logits, void* stream) {
+    g_err.clear();
+    if (int rc = check_dtype(dtype)) return rc;
+    if (T < 0) return fail(ELB_ERR_INVALID_ARG, "T = %lld < 0", (long long)T);
+    if (N < 2) return fail(ELB_ERR_INVALID_ARG, "N = %d: need at least 2 experts", N);
+    if (N > ELB_MAX_EXPERTS) return fail(ELB_ERR_UNSUPPORTED, "N = %d exceeds %d", N, ELB_MAX_EXPERTS);
+    if (d < 1) return fail(ELB_ERR_INVALID_ARG, "d = %d < 1", d);
+    if (dtype == ELB_BF16 && d % 32)
+        return fail(ELB_ERR_INVALID_ARG, "bf16 router needs d %% 32 == 0 (d = %d)", d);
+    if (T == 0) return ELB_OK;
+    if (!x || !W_router || !logits) return fail(ELB_ERR_INVALID_ARG, "NULL tensor pointer");
+    return hip_status(launch_router(x, W_router, T, d, N, dtype, logits, (hipStream_t)stream),
+                      "router");
+}
+
+int elb_route(const float* logits, int64_t T, int32_t N, const elb_route_params* params,
+              int32_t* k, int32_t* ids, float* w, void* stream) {
+    g_err.clear();
+    if (T < 0) return fail(ELB_ERR_INVALID_ARG, "T = %lld < 0", (long long)T);
+    if (int rc = check_route_params(N, params)) return rc;
+    if (T == 0) return ELB_OK;
+    if (!logits || !k || !ids || !w) return fail(ELB_ERR_INVALID_ARG, "NULL tensor pointer");
+    return hip_status(launch_route(logits, T, N, *params, k, ids, w, (hipStream_t)stream),
+                      "route");
+}
+
+size_t elb_dispatch_workspace_bytes(int64_t T, int32_t N) {
+    if (T < 0 || N < 1) return 0;
+    return align_up((size_t)dispatch_groups(T) * N * 4) + align_up((size_t)(N + 1) * 4);
+}
+
+int elb_dispatch(const int32_t* k, const int32_t* ids, int64_t T, int32_t N, int32_t K,
+                 int32_t* counts, int32_t* offsets, int32_t* row_token, int32_t* inv,
+                 void* workspace, size_t workspace_bytes, void* stream) {
+    g_err.clear();
+    if (T < 0) return fail(ELB_ERR_INVALID_ARG, "T = %lld < 0", (long long)T);
+    if (N < 2) return fail(ELB_ERR_INVALID_ARG, "N = %d: need at least 2 experts", N);
+    if (N > ELB_MAX_EXPERTS) return fail(ELB_ERR_UNSUPPORTED, "N = %d exceeds %d", N, ELB_MAX_EXPERTS);
+    if (K < 1 || K > N) return fail(ELB_ERR_INVALID_ARG, "K = %d outside [1, N = %d]", K, N);
+    if (T * (int64_t)K >= (int64_t)1 << 31)
+        return fail(ELB_ERR_UNSUPPORTED, "T * K exceeds 2^31");
+    if (!counts || !offsets) return fail(ELB_ERR_INVALID_ARG, "NULL tensor pointer");
+    if (T > 0 && (!k || !ids || !row_token || !inv))
+        return fail(ELB_ERR_INVALID_ARG, "NULL tensor pointer");
+    const size_t need = elb_dispatch_workspace_bytes(T, N);
+    if (!workspace || workspace_bytes < need)
+        return fail(ELB_ERR_WORKSPACE, "workspace of %zu bytes, need %zu", workspace_bytes, need);
+    char* ws = (char*)workspace;
+    int* hist = (int*)ws;
+    int* tile_off = (int*)(ws + align_up((size_t)dispatch_groups(T) * N * 4));
+    return hip_status(launch_dispatch(k, ids, T, N, K, counts, offsets, row_token, inv, hist,
+                                      tile_off, gemm_tile_rows(ELB_BF16), (hipStream_t)stream),
+                      "dispatch");
+}
+
+size_t elb_moe_workspace_bytes(int64_t T, int32_t d, int32_t N, int32_t m, int32_t K,
+                               int32_t dtype) {
+    if (T < 0 || d < 1 || N < 1 || m < 1 || K < 1 || (dtype != ELB_F32 && dtype != ELB_BF16))
+        return 0;
+    return layout(T, d, N, m, K, dtype).total;
+}
+
+static int experts_impl(const void* x, const void* W_gate_up, const void* W_down,
+                        const int32_t* k, const int32_t* ids, const float* w,
+                        const void* residual, int64_t T, int d, int N, int m, int K, int dtype,
+                        void* y, char* ws, const Layout& L, int32_t* counts_out,
+                        hipStream_t s) {
+    int* hist = (int*)(ws + L.hist);
+    int* tile_off = (int*)(ws + L.tile_off);
+    int* counts = counts_out ? counts_out : (int*)(ws + L.counts);
+    int* offsets = (int*)(ws + L.offsets);
+    int* row_token = (int*)(ws + L.row_token);
+    int* inv = (int*)(ws + L.inv);
+    void* H = ws + L.H;
+    void* Y = ws + L.Y;
+    const int tr = gemm_tile_rows(dtype);
+    const int64_t mt = max_tiles(T, K, N, tr);
+    if (int rc = hip_status(launch_dispatch(k, ids, T, N, K, counts, offsets, row_token, inv,
+                                            hist, tile_off, tr, s), "dispatch"))
+        return rc;
+    if (int rc = hip_status(launch_gemm_gate_up(x, W_gate_up, row_token, offsets, tile_off, mt,
+                                                d, N, m, dtype, H, s), "gemm_gate_up"))
+        return rc;
+    if (int rc = hip_status(launch_gemm_down(H, W_down, offsets, tile_off, mt, d, N, m, dtype,
+                                             Y, s), "gemm_down"))
+        return rc;
+    return hip_status(launch_combine(Y, k, inv, w, residual, T, d, K, dtype, y, s), "combine");
+}
+
+int elb_moe_experts(const void* x, const void* W_gate_up, const void* W_down,
+                    const int32_t* k, const int32_t* ids, const float* w, const void* residual,
+                    int64_t T, int32_t d, int32_t N, int32_t m, int32_t K, int32_t dtype,
+                    void* y, void* workspace, size_t workspace_bytes, void* stream) {
+    g_err.clear();
+    if (int rc = check_expert_dims(T, d, N, m, K, dtype)) return rc;
+    if (T == 0) return ELB_OK;
+    if (!x || !W_gate_up || !W_down || !k || !ids || !w || !y)
+        return fail(ELB_ERR_INVALID_ARG, "NULL tensor pointer");
+    const Layout L = layout(T, d, N, m, K, dtype);
+    if (!workspace || workspace_bytes < L.experts_end)
+        return fail(ELB_ERR_WORKSPACE, "workspace of %zu bytes, need %zu", workspace_bytes,
+                    L.experts_end);
+    return experts_impl(x, W_gate_up, W_down, k, ids, w, residual, T, d, N, m, K, dtype, y,
+                        (char*)workspace, L, nullptr, (hipStream_t)stream);
+}
+
+int elb_moe_forward(const void* x, const void* W_router, const void* W_gate_up,
+                    const void* W_down, const void* residual, int64_t T, int32_t d, int32_t N,
+                    int32_t m, int32_t dtype, const elb_route_params* params, void* y,
+                    void* workspace, size_t workspace_bytes, float* logits_out,
+                    int32_t* k_out, int32_t* ids_out, float* w_out, int32_t* counts_out,
+                    void* stream) {
+    g_err.clear();
+    if (int rc = check_route_params(N, params)) return rc;
+    if (int rc = check_expert_dims(T, d, N, m, params->K, dtype)) return rc;
+    if (T == 0) return ELB_OK;
+    if (!x || !W_router || !W_gate_up || !W_down || !y)
+        return fail(ELB_ERR_INVALID_ARG, "NULL tensor pointer");
+    const int K = params->K;
+    const Layout L = layout(T, d, N, m, K, dtype);
+    if (!workspace || workspace_bytes < L.total)
+        return fail(ELB_ERR_WORKSPACE, "workspace of %zu bytes, need %zu", workspace_bytes,
+                    L.total);
+    char* ws = (char*)workspace;
+    hipStream_t s = (hipStream_t)stream;
+    float* logits = logits_out ? logits_out : (float*)(ws + L.logits);
+    int* k = k_out ? k_out : (int*)(ws + L.k);
+    int* ids = ids_out ? ids_out : (int*)(ws + L.ids);
+    float* w = w_out ? w_out : (float*)(ws + L.w);
+    if (int rc = hip_status(launch_router(x, W_router, T, d, N, dtype, logits, s), "router"))
+        return rc;
+    if (int rc = hip_status(launch_route(logits, T, N, *params, k, ids, w, s), "route"))
+        return rc;
+    return experts_impl(x, W_gate_up, W_down, k, ids, w, residual, T, d, N, m, K, dtype, y, ws,
+                        L, counts_out, s);
+}
+
+int elb_profile_enable(int on) {
+    g_prof_on.store(on != 0);
+    return ELB_OK;
+}
+
+int elb_profile_read(const char** names, double* total_ms, int64_t* launches, int cap) {
+    std::lock_guard<std::mutex> lk(g_prof_mu);
+    std::map<std::string, std::pair<double, int64_t>> acc;
+    int rc = ELB_OK;
+    for (Rec& r : g_recs) {
+        float ms = 0.f;
+        if (hipEventSynchronize(r.b) != hipSuccess ||
+            hipEventElapsedTime(&ms, r.a, r.b) != hipSuccess)
+            rc = ELB_ERR_HIP;
+        auto it = acc.find(r.name);
+        if (it == acc.end()) {
+            acc[r.name] = {ms, 1};
+        } else {
+            it->second.first += ms;
+            it->second.second += 1;
+        }
+        g_pool.push_back(r.a);
+        g_pool.push_back(r.b);
+    }
+    std::vector<const char*> static_names;
+    for (Rec& r : g_recs)
+        if (std::find(static_names.begin(), static_names.end(), r.name) == static_names.end())
+            static_names.push_back(r.name);
+    g_recs.clear();
+    if (rc != ELB_OK) return -fail(rc, "profile events failed");
+    int n = 0;
+    for (const char* nm : static_names) {
+        if (n < cap) {
+            if (names) names[n] = nm;
+            if (total_ms) total_ms[n] = acc[nm].first;
+            if (launches) launches[n] = acc[nm].second;
+        }
+        ++n;
+    }
+    return n;
+}
+
+}  // extern "C"

@@ -1,0 +1,93 @@
+// Weighted combine of the expert outputs back to token order (the MoE output is the
+// routing-weighted sum over the token's selected experts, Section 2):
+//   y[t] = [residual[t] +] sum_{j < k_t} w[t, j] * Y[inv[t, j]]
+// summed in rank order j = 0, 1, ... with fp32 accumulation (deterministic; no atomics).
+// y may alias residual (each element is read, then written, by the same thread).
+// One block per token; each thread owns 8 (bf16) or 4 (fp32) consecutive columns, so every
+// expert row is read with 16-byte coalesced loads.
+#include "common.h"
+
+namespace elb {
+
+namespace {
+
+__global__ __launch_bounds__(256) void combine_bf16(const bf16_t* __restrict__ Y,
+                                                    const int* __restrict__ k,
+                                                    const int* __restrict__ inv,
+                                                    const float* __restrict__ w,
+                                                    const bf16_t* residual,
+                                                    int64_t T, int d, int K, bf16_t* y) {
+    const int64_t t = blockIdx.x;
+    const int kt = k[t];
+    for (int c = threadIdx.x * 8; c < d; c += 256 * 8) {
+        float acc[8];
+        if (residual) {
+            const uint4 q = *reinterpret_cast<const uint4*>(residual + t * d + c);
+            const bf16_t* h = reinterpret_cast<const bf16_t*>(&q);
+#pragma unroll
+            for (int i = 0; i < 8; ++i) acc[i] = bf16_to_f32(h[i]);
+        } else {
+#pragma unroll
+            for (int i = 0; i < 8; ++i) acc[i] = 0.f;
+        }
+        for (int j = 0; j < kt && j < K; ++j) {
+            const int r = inv[t * K + j];
+            if (r < 0) continue;
+            const float wj = w[t * K + j];
+            const uint4 q = *reinterpret_cast<const uint4*>(Y + (int64_t)r * d + c);
+            const bf16_t* h = reinterpret_cast<const bf16_t*>(&q);
+#pragma unroll
+            for (int i = 0; i < 8; ++i) acc[i] = fmaf(wj, bf16_to_f32(h[i]), acc[i]);
+        }
+        uint4 o;
+        bf16_t* ob = reinterpret_cast<bf16_t*>(&o);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) ob[i] = f32_to_bf16(acc[i]);
+        *reinterpret_cast<uint4*>(y + t * d + c) = o;
+    }
+}
+
+__global__ __launch_bounds__(256) void combine_f32(const float* __restrict__ Y,
+                                                   const int* __restrict__ k,
+                                                   const int* __restrict__ inv,
+                                                   const float* __restrict__ w,
+                                                   const float* residual,
+                                                   int64_t T, int d, int K, float* y) {
+    const int64_t t = blockIdx.x;
+    const int kt = k[t];
+    for (int c = threadIdx.x * 4; c < d; c += 256 * 4) {
+        float4 acc = residual ? *reinterpret_cast<const float4*>(residual + t * d + c)
+                              : make_float4(0.f, 0.f, 0.f, 0.f);
+        for (int j = 0; j < kt && j < K; ++j) {
+            const int r = inv[t * K + j];
+            if (r < 0) continue;
+            const float wj = w[t * K + j];
+            const float4 q = *reinterpret_cast<const float4*>(Y + (int64_t)r * d + c);
+            acc.x = fmaf(wj, q.x, acc.x);
+            acc.y = fmaf(wj, q.y, acc.y);
+            acc.z = fmaf(wj, q.z, acc.z);
+            acc.w = fmaf(wj, q.w, acc.w);
+        }
+        *reinterpret_cast<float4*>(y + t * d + c) = acc;
+    }
+}
+
+}  // namespace
+
+hipError_t launch_combine(const void* Y, const int* k, const int* inv, const float* w,
+                          const void* residual, int64_t T, int d, int K, int dtype, void* y,
+                          hipStream_t s) {
+    if (T == 0) return hipSuccess;
+    if (dtype == ELB_BF16) {
+        ProfileScope prof("combine_bf16", s);
+        hipLaunchKernelGGL(combine_bf16, dim3((unsigned)T), dim3(256), 0, s, (const bf16_t*)Y, k,
+                           inv, w, (const bf16_t*)residual, T, d, K, (bf16_t*)y);
+    } else {
+        ProfileScope prof("combine_f32", s);
+        hipLaunchKernelGGL(combine_f32, dim3((unsigned)T), dim3(256), 0, s, (const float*)Y, k,
+                           inv, w, (const float*)residual, T, d, K, (float*)y);
+    }
+    return hipGetLastError();
+}
+
+}  // namespace elb

@@ -1,0 +1,71 @@
+// Internal declarations shared by the HIP sources of libelbow_moe (not part of the ABI).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/elbow_moe.h"
+
+namespace elb {
+
+// bf16 is stored as uint16 (the upper half of an fp32 bit pattern).
+typedef uint16_t bf16_t;
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ float bf16_to_f32(bf16_t v) {
+    return __uint_as_float(((uint32_t)v) << 16);
+}
+
+// round to nearest even (finite inputs; NaN keeps a quiet NaN pattern)
+__device__ __forceinline__ bf16_t f32_to_bf16(float f) {
+    uint32_t u = __float_as_uint(f);
+    if ((u & 0x7fffffffu) > 0x7f800000u) return (bf16_t)((u >> 16) | 0x40);
+    u += 0x7fffu + ((u >> 16) & 1u);
+    return (bf16_t)(u >> 16);
+}
+
+constexpr int kWave = 64;
+
+// ---- kernel launchers (defined in the .hip files); each returns hipGetLastError() ----
+
+// routing: logits [T, N] -> k [T], ids [T, K], w [T, K]
+hipError_t launch_route(const float* logits, int64_t T, int N, const elb_route_params& p,
+                        int* k, int* ids, float* w, hipStream_t s);
+
+// dispatch: number of 64-token groups and the workspace it needs
+inline int64_t dispatch_groups(int64_t T) { return (T + kWave - 1) / kWave; }
+// hist [groups, N] int32 scratch; tile_off [N + 1] (tiles of `tile_rows` rows per expert)
+hipError_t launch_dispatch(const int* k, const int* ids, int64_t T, int N, int K, int* counts,
+                           int* offsets, int* row_token, int* inv, int* hist, int* tile_off,
+                           int tile_rows, hipStream_t s);
+
+// router logits
+hipError_t launch_router(const void* x, const void* Wr, int64_t T, int d, int N, int dtype,
+                         float* logits, hipStream_t s);
+
+// grouped GEMMs
+int gemm_tile_rows(int dtype);  // rows per M-tile used by the grouped GEMMs
+hipError_t launch_gemm_gate_up(const void* x, const void* Wgu, const int* row_token,
+                               const int* offsets, const int* tile_off, int64_t max_tiles,
+                               int d, int N, int m, int dtype, void* H, hipStream_t s);
+hipError_t launch_gemm_down(const void* H, const void* Wd, const int* offsets,
+                            const int* tile_off, int64_t max_tiles, int d, int N, int m,
+                            int dtype, void* Y, hipStream_t s);
+
+// combine: y[t] = residual[t] + sum_j w[t, j] Y[inv[t, j]]
+hipError_t launch_combine(const void* Y, const int* k, const int* inv, const float* w,
+                          const void* residual, int64_t T, int d, int K, int dtype, void* y,
+                          hipStream_t s);
+
+// ---- per-kernel timing hooks (api.hip) ----
+struct ProfileScope {
+    ProfileScope(const char* name, hipStream_t s);
+    ~ProfileScope();
+    const char* name_;
+    hipStream_t s_;
+    int slot_;
+};
+
+}  // namespace elb

@@ -1,0 +1,110 @@
+"""The C-ABI library: it loads, exports every entry point declared in include/elbow_moe.h,
+and rejects invalid arguments on the host before anything is launched (no GPU needed:
+validation runs before any HIP call, and the dummy pointers below are never dereferenced).
+"""
+import ctypes as C
+import os
+import re
+
+import pytest
+
+from paper_2608_04401_amd import binding as B
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "elbow_moe.h")
+
+OK, INVALID, UNSUPPORTED, WORKSPACE = 0, 1, 2, 3
+DUMMY = C.c_void_p(0x1000)   # never dereferenced: every call below fails validation
+
+
+def declared_functions():
+    txt = open(HEADER).read()
+    txt = re.sub(r"/\*.*?\*/", "", txt, flags=re.S)
+    return sorted(set(re.findall(r"\b(elb_[a-z_]+)\s*\(", txt)))
+
+
+def test_library_exports_every_declared_symbol():
+    lib = B.lib()
+    names = declared_functions()
+    assert len(names) >= 12
+    for n in names:
+        assert hasattr(lib, n), n
+    assert B.elb_abi_version() == 1
+
+
+def test_status_strings():
+    lib = B.lib()
+    assert lib.elb_status_str(0) == b"ELB_OK"
+    assert lib.elb_status_str(3) == b"ELB_ERR_WORKSPACE"
+    assert lib.elb_status_str(99) == b"ELB_ERR_UNKNOWN"
+
+
+def _route(T, N, K=8, eps=1e-8, mode=0, renorm=0, ptr=DUMMY, params=True):
+    p = B.RouteParams(K, eps, mode, renorm)
+    return B.lib().elb_route(ptr, T, N, C.byref(p) if params else None, ptr, ptr, ptr, None)
+
+
+@pytest.mark.parametrize("T,N,K,eps,mode,renorm,want", [
+    (-1, 64, 8, 1e-8, 0, 0, INVALID),        # negative T
+    (10, 1, 1, 1e-8, 0, 0, INVALID),         # N < 2
+    (10, 65, 8, 1e-8, 0, 0, UNSUPPORTED),    # N beyond the kernels
+    (10, 64, 0, 1e-8, 0, 0, INVALID),        # K < 1
+    (10, 8, 9, 1e-8, 0, 0, INVALID),         # K > N
+    (10, 64, 17, 1e-8, 0, 0, UNSUPPORTED),   # K beyond the kernels
+    (10, 64, 8, -1.0, 0, 0, INVALID),        # eps < 0
+    (10, 64, 8, float("nan"), 0, 0, INVALID),
+    (10, 64, 8, 1e-8, 2, 0, INVALID),        # bad mode
+    (10, 64, 8, 1e-8, 0, 2, INVALID),        # bad renormalize flag
+])
+def test_route_validation(T, N, K, eps, mode, renorm, want):
+    assert _route(T, N, K, eps, mode, renorm) == want
+    assert B.lib().elb_last_error() != b""
+
+
+def test_route_null_and_empty():
+    assert _route(10, 64, params=False) == INVALID
+    assert _route(10, 64, ptr=None) == INVALID
+    assert _route(0, 64, ptr=None) == OK          # T = 0: nothing to do, nothing launched
+
+
+def test_experts_validation():
+    lib = B.lib()
+    f = lib.elb_moe_experts
+
+    def call(T=16, d=128, N=8, m=128, K=4, dt=1, ws=DUMMY, wsb=1 << 40, y=DUMMY):
+        return f(DUMMY, DUMMY, DUMMY, DUMMY, DUMMY, DUMMY, None, T, d, N, m, K, dt, y, ws, wsb,
+                 None)
+    assert call(d=96) == INVALID                  # bf16 needs d % 64 == 0
+    assert call(m=100, dt=0) == INVALID           # f32 needs m % 16 == 0
+    assert call(dt=7) == INVALID
+    assert call(N=80) == UNSUPPORTED
+    assert call(K=9) == INVALID
+    assert call(ws=None) == WORKSPACE
+    assert call(wsb=16) == WORKSPACE
+    assert call(y=None) == INVALID
+    assert call(T=0, ws=None, y=None) == OK
+
+
+def test_workspace_sizes():
+    lib = B.lib()
+    small = lib.elb_moe_workspace_bytes(256, 128, 8, 256, 8, 0)
+    big = lib.elb_moe_workspace_bytes(4096, 2048, 64, 1024, 8, 1)
+    assert 0 < small < big
+    # H and Y dominate: T K (m + d) bf16 elements
+    assert big >= 4096 * 8 * (1024 + 2048) * 2
+    assert lib.elb_moe_workspace_bytes(-1, 128, 8, 256, 8, 0) == 0
+    assert lib.elb_dispatch_workspace_bytes(65536, 64) >= 1024 * 64 * 4
+
+
+def test_dispatch_and_router_validation():
+    lib = B.lib()
+    assert lib.elb_dispatch(DUMMY, DUMMY, 100, 64, 8, DUMMY, DUMMY, DUMMY, DUMMY, DUMMY, 4,
+                            None) == WORKSPACE
+    assert lib.elb_dispatch(DUMMY, DUMMY, 100, 64, 65, DUMMY, DUMMY, DUMMY, DUMMY, DUMMY,
+                            1 << 30, None) == INVALID
+    assert lib.elb_router_logits(DUMMY, DUMMY, 100, 100, 64, 1, DUMMY, None) == INVALID
+    assert lib.elb_router_logits(DUMMY, DUMMY, 100, 128, 100, 1, DUMMY, None) == UNSUPPORTED
+
+
+def test_profile_read_empty():
+    assert B.elb_profile_read() == {}

@@ -1,0 +1,188 @@
+"""GPU parity: dispatch, router GEMM, grouped SwiGLU expert GEMMs, combine and the whole
+layer, through the C ABI, against the fp64 oracle on identical seeded inputs."""
+import numpy as np
+import pytest
+import torch
+
+from oracle import oracle as O
+from paper_2608_04401_amd import binding as B
+from paper_2608_04401_amd import synth
+
+from helpers import (NEAR_TIE, RTOL_BF16, RTOL_F32, compare_routing, cpu, rel_err_rows,
+                     to_gpu)
+
+pytestmark = pytest.mark.gpu
+BF = torch.bfloat16
+
+
+def _layer_gpu(L, dtype):
+    return tuple(to_gpu(a, dtype) for a in (L.x, L.W_router, L.W_gu, L.W_down))
+
+
+@pytest.fixture(scope="module")
+def olmoe():
+    """OLMoE-shaped prefill layer: T=4096, d=2048, N=64 experts, intermediate 1024, bf16."""
+    L = synth.olmoe_layer(T=4096, seed=0)
+    lg64 = O.router_logits(L.x, L.W_router)
+    return L, lg64, _layer_gpu(L, BF)
+
+
+# ------------------------------------------------------------------------------ dispatch
+@pytest.mark.parametrize("T,N,K", [(65536, 64, 8), (1000, 64, 8), (777, 5, 3), (64, 8, 8),
+                                   (1, 2, 1), (4096, 33, 16)])
+def test_dispatch_matches_oracle(T, N, K):
+    lg = synth.planted_logits(T, N, seed=T + N, m_max=min(8, N))
+    r = O.route(lg, K=K)
+    counts, offsets, row_token, inv = B.elb_dispatch(to_gpu(r.k, torch.int32),
+                                                     to_gpu(r.ids, torch.int32), N)
+    c0, o0, rt0, inv0 = O.dispatch(r.k, r.ids, N)
+    assert np.array_equal(cpu(counts), c0)
+    assert np.array_equal(cpu(offsets), o0)
+    assert np.array_equal(cpu(row_token)[:len(rt0)], rt0)
+    assert (cpu(row_token)[len(rt0):] == -1).all()        # rows past sum k untouched
+    assert np.array_equal(cpu(inv), inv0)
+
+
+def test_dispatch_topk_and_ids_outside_selection():
+    lg = synth.gaussian_logits(3000, 64, seed=2)
+    r = O.route(lg, K=8, mode=O.MODE_TOPK)
+    out = B.elb_dispatch(to_gpu(r.k, torch.int32), to_gpu(r.ids, torch.int32), 64)
+    ref = O.dispatch(r.k, r.ids, 64)
+    for a, b in zip(out[:2], ref[:2]):
+        assert np.array_equal(cpu(a), b)
+    assert np.array_equal(cpu(out[3]), ref[3])
+
+
+# ------------------------------------------------------------------------------ router
+def test_router_logits_bf16(olmoe):
+    L, lg64, (x, Wr, _, _) = olmoe
+    lg = cpu(B.elb_router_logits(x, Wr))
+    rel = rel_err_rows(lg, lg64)
+    assert rel.max() < 1e-5, rel.max()
+
+
+def test_router_logits_f32_tiny():
+    L = synth.tiny_layer(seed=0)
+    lg = cpu(B.elb_router_logits(to_gpu(L.x), to_gpu(L.W_router)))
+    assert rel_err_rows(lg, O.router_logits(L.x, L.W_router)).max() < 1e-5
+
+
+def test_router_ragged_tokens_and_experts():
+    L = synth.moe_layer(37, 96, 50, 64, dtype="bf16", seed=3)
+    lg = cpu(B.elb_router_logits(to_gpu(L.x, BF), to_gpu(L.W_router, BF)))
+    assert rel_err_rows(lg, O.router_logits(L.x, L.W_router)).max() < 1e-5
+
+
+# ------------------------------------------------------------------------------ experts
+def _experts_case(L, dtype, K, mode, rtol, sample=None, residual=None, seed=0):
+    """Expert part with the ORACLE's routing (from its fp64 logits) fed to both sides."""
+    lg64 = O.router_logits(L.x, L.W_router)
+    r = O.route(lg64.astype(np.float32), K=K, mode=mode)
+    x, _, Wgu, Wd = _layer_gpu(L, dtype)
+    res_g = None if residual is None else to_gpu(residual, dtype)
+    y = B.elb_moe_experts(x, Wgu, Wd, to_gpu(r.k, torch.int32), to_gpu(r.ids, torch.int32),
+                          to_gpu(r.w.astype(np.float32)), residual=res_g)
+    torch.cuda.synchronize()
+    tok = np.arange(L.T) if sample is None else np.sort(
+        np.random.default_rng(seed).choice(L.T, sample, replace=False))
+    ref = O.moe_experts(L.x, L.W_gu, L.W_down, r.k[tok], r.ids[tok],
+                        r.w[tok].astype(np.float32).astype(np.float64), tokens=tok,
+                        residual=residual)
+    rel = rel_err_rows(cpu(y)[tok], ref)
+    print("experts: dtype %s K %d mode %d: tokens %d, max rel %.3e, mean rel %.3e" % (
+        dtype, K, mode, len(tok), rel.max(), rel.mean()))
+    assert rel.max() < rtol, rel.max()
+    return y
+
+
+def test_experts_f32_tiny():
+    _experts_case(synth.tiny_layer(seed=0), torch.float32, 8, O.MODE_ELBOW, RTOL_F32)
+
+
+def test_experts_f32_ragged():
+    L = synth.moe_layer(333, 48, 5, 80, dtype="f32", seed=4)
+    _experts_case(L, torch.float32, 3, O.MODE_ELBOW, RTOL_F32)
+    _experts_case(L, torch.float32, 5, O.MODE_TOPK, RTOL_F32)
+
+
+def test_experts_bf16_ragged_with_residual():
+    L = synth.moe_layer(300, 192, 16, 320, dtype="bf16", seed=5)
+    res = synth.round_bf16(synth.gaussian_logits(300, 192, seed=6))
+    _experts_case(L, BF, 4, O.MODE_ELBOW, RTOL_BF16, residual=res)
+
+
+@pytest.mark.parametrize("mode", [O.MODE_ELBOW, O.MODE_TOPK])
+def test_experts_bf16_olmoe_sampled(olmoe, mode):
+    L = olmoe[0]
+    _experts_case(L, BF, 8, mode, RTOL_BF16, sample=96, seed=mode)
+
+
+# ------------------------------------------------------------------------------ whole layer
+def _forward_case(L, dtype, K, mode, rtol, sample=None, seed=0):
+    x, Wr, Wgu, Wd = _layer_gpu(L, dtype)
+    y, dbg = B.elb_moe_forward(x, Wr, Wgu, Wd, K=K, mode=mode, debug=True)
+    torch.cuda.synchronize()
+    tok = np.arange(L.T) if sample is None else np.sort(
+        np.random.default_rng(seed).choice(L.T, sample, replace=False))
+    ref = O.moe_forward(L.x, L.W_router, L.W_gu, L.W_down, K=K, mode=mode, tokens=tok)
+    # logits
+    assert rel_err_rows(cpu(dbg["logits"])[tok], ref.logits).max() < 1e-5
+    # routing vs the oracle's routing on its own fp64 logits
+    k, ids = cpu(dbg["k"])[tok], cpu(dbg["ids"])[tok]
+    same = (k == ref.routing.k) & (ids == ref.routing.ids).all(axis=1)
+    assert (ref.routing.margin[~same] < NEAR_TIE).all()
+    # outputs on tokens routed identically
+    rel = rel_err_rows(cpu(y)[tok][same], ref.y[same])
+    print("forward: T %d K %d mode %d: compared %d tokens, routing near-tie mismatches %d, "
+          "max rel %.3e" % (L.T, K, mode, int(same.sum()), int((~same).sum()), rel.max()))
+    assert rel.max() < rtol, rel.max()
+    # counts output = assignments per expert of the routing the layer used
+    counts = cpu(dbg["counts"])
+    kk, ii = cpu(dbg["k"]), cpu(dbg["ids"])
+    assert counts.sum() == kk.sum()
+    assert np.array_equal(counts, np.bincount(ii[ii >= 0], minlength=L.N))
+    return y, dbg
+
+
+def test_forward_f32_tiny_all_tokens():
+    _forward_case(synth.tiny_layer(seed=0), torch.float32, 8, O.MODE_ELBOW, RTOL_F32)
+    _forward_case(synth.tiny_layer(seed=1), torch.float32, 2, O.MODE_ELBOW, RTOL_F32)
+
+
+@pytest.mark.parametrize("mode", [O.MODE_ELBOW, O.MODE_TOPK])
+def test_forward_bf16_olmoe_prefill_sampled(olmoe, mode):
+    L = olmoe[0]
+    y, dbg = _forward_case(L, BF, 8, mode, RTOL_BF16, sample=96, seed=10 + mode)
+    if mode == O.MODE_ELBOW:
+        print("prefill mean k %.4f" % cpu(dbg["k"]).mean())
+
+
+def test_forward_bf16_decode_all_tokens():
+    L = synth.olmoe_layer(T=64, seed=2)
+    _forward_case(L, BF, 8, O.MODE_ELBOW, RTOL_BF16)
+
+
+def test_forward_deterministic(olmoe):
+    _, _, (x, Wr, Wgu, Wd) = olmoe
+    y1 = B.elb_moe_forward(x, Wr, Wgu, Wd, K=8)
+    y2 = B.elb_moe_forward(x, Wr, Wgu, Wd, K=8)
+    torch.cuda.synchronize()
+    assert torch.equal(y1.view(torch.int16), y2.view(torch.int16))
+
+
+def test_forward_residual_stack_two_layers():
+    """Two residual layers h <- h + MoE_l(h), compared layer by layer on the same input
+    (teacher-forced): the input of layer 2 is the oracle's layer-1 output rounded to bf16."""
+    T, d, N, m = 256, 128, 8, 64
+    h = synth.round_bf16(synth.gaussian_logits(T, d, seed=21))
+    for l in range(2):
+        L = synth.moe_layer(T, d, N, m, dtype="bf16", seed=[21, l], with_x=False)
+        hg = to_gpu(h, BF)
+        y = B.elb_moe_forward(hg, to_gpu(L.W_router, BF), to_gpu(L.W_gu, BF),
+                              to_gpu(L.W_down, BF), K=4, residual=hg)
+        torch.cuda.synchronize()
+        ref = O.moe_forward(h, L.W_router, L.W_gu, L.W_down, K=4, residual=h)
+        rel = rel_err_rows(cpu(y), ref.y)
+        near = ref.routing.margin < NEAR_TIE
+        assert rel[~near].max() < RTOL_BF16
+        h = synth.round_bf16(ref.y.astype(np.float32))
