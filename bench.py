@@ -121,6 +121,7 @@ def main():
     ap.add_argument("--workload", default="olmoe-prefill", choices=sorted(WORKLOADS))
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-routing", action="store_true")
+    ap.add_argument("--no-topk", action="store_true", help="skip the fixed top-K baseline")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path "
@@ -152,8 +153,11 @@ def main():
 
     log("timing elbow layer: %d warmup, %d steps" % (args.warmup, args.steps))
     ms, kern = time_layer(B, torch, gpu, K, B.MODE_ELBOW, args.steps, args.warmup, True)
-    log("timing top-8 baseline")
-    ms_top, kern_top = time_layer(B, torch, gpu, K, B.MODE_TOPK, args.steps, args.warmup, True)
+    ms_top, kern_top = None, {}
+    if not args.no_topk:
+        log("timing top-8 baseline")
+        ms_top, kern_top = time_layer(B, torch, gpu, K, B.MODE_TOPK, args.steps, args.warmup,
+                                      True)
     # same timed loop without the per-kernel events, for the event overhead
     ms_noev, _ = time_layer(B, torch, gpu, K, B.MODE_ELBOW, args.steps, 2, False)
 
@@ -195,10 +199,12 @@ def main():
             kern[n] for n in kern if n.startswith("gemm")) * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
         "kernels_us": {n: round(v * 1e3, 2) for n, v in kern.items()},
         "ms_per_step_without_kernel_events": round(ms_noev, 4),
-        "topk_baseline": {"value": round(T / (ms_top * 1e-3), 1), "unit": "tokens/s",
-                          "ms_per_step": round(ms_top, 4), "sum_k": sum_k_top,
-                          "kernels_us": {n: round(v * 1e3, 2) for n, v in kern_top.items()}},
-        "elbow_vs_topk_latency_change_pct": round((ms - ms_top) / ms_top * 100, 2),
+        "topk_baseline": None if ms_top is None else {
+            "value": round(T / (ms_top * 1e-3), 1), "unit": "tokens/s",
+            "ms_per_step": round(ms_top, 4), "sum_k": sum_k_top,
+            "kernels_us": {n: round(v * 1e3, 2) for n, v in kern_top.items()}},
+        "elbow_vs_topk_latency_change_pct": None if ms_top is None else round(
+            (ms - ms_top) / ms_top * 100, 2),
         "paper_context": "the paper reports a 5.3% average latency reduction on OLMoE on one "
                          "NVIDIA H200 (context only)",
     }

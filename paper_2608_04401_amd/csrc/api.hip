@@ -233,7 +233,7 @@ int elb_dispatch(const int32_t* k, const int32_t* ids, int64_t T, int32_t N, int
     int* hist = (int*)ws;
     int* tile_off = (int*)(ws + align_up((size_t)dispatch_groups(T) * N * 4));
     return hip_status(launch_dispatch(k, ids, T, N, K, counts, offsets, row_token, inv, hist,
-                                      tile_off, gemm_tile_rows(ELB_BF16), (hipStream_t)stream),
+                                      tile_off, 128, (hipStream_t)stream),
                       "dispatch");
 }
 
@@ -257,16 +257,16 @@ static int experts_impl(const void* x, const void* W_gate_up, const void* W_down
     int* inv = (int*)(ws + L.inv);
     void* H = ws + L.H;
     void* Y = ws + L.Y;
-    const int tr = gemm_tile_rows(dtype);
+    const int tr = gemm_tile_rows(dtype, T, K, N, m);
     const int64_t mt = max_tiles(T, K, N, tr);
     if (int rc = hip_status(launch_dispatch(k, ids, T, N, K, counts, offsets, row_token, inv,
                                             hist, tile_off, tr, s), "dispatch"))
         return rc;
     if (int rc = hip_status(launch_gemm_gate_up(x, W_gate_up, row_token, offsets, tile_off, mt,
-                                                d, N, m, dtype, H, s), "gemm_gate_up"))
+                                                tr, d, N, m, dtype, H, s), "gemm_gate_up"))
         return rc;
-    if (int rc = hip_status(launch_gemm_down(H, W_down, offsets, tile_off, mt, d, N, m, dtype,
-                                             Y, s), "gemm_down"))
+    if (int rc = hip_status(launch_gemm_down(H, W_down, offsets, tile_off, mt, tr, d, N, m,
+                                             dtype, Y, s), "gemm_down"))
         return rc;
     return hip_status(launch_combine(Y, k, inv, w, residual, T, d, K, dtype, y, s), "combine");
 }

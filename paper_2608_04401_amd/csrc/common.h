@@ -46,13 +46,15 @@ hipError_t launch_router(const void* x, const void* Wr, int64_t T, int d, int N,
                          float* logits, hipStream_t s);
 
 // grouped GEMMs
-int gemm_tile_rows(int dtype);  // rows per M-tile used by the grouped GEMMs
+// rows per M-tile of the grouped GEMMs for this problem (the dispatch scan uses the same)
+int gemm_tile_rows(int dtype, int64_t T, int K, int N, int m);
 hipError_t launch_gemm_gate_up(const void* x, const void* Wgu, const int* row_token,
                                const int* offsets, const int* tile_off, int64_t max_tiles,
-                               int d, int N, int m, int dtype, void* H, hipStream_t s);
+                               int tile_rows, int d, int N, int m, int dtype, void* H,
+                               hipStream_t s);
 hipError_t launch_gemm_down(const void* H, const void* Wd, const int* offsets,
-                            const int* tile_off, int64_t max_tiles, int d, int N, int m,
-                            int dtype, void* Y, hipStream_t s);
+                            const int* tile_off, int64_t max_tiles, int tile_rows, int d, int N,
+                            int m, int dtype, void* Y, hipStream_t s);
 
 // combine: y[t] = residual[t] + sum_j w[t, j] Y[inv[t, j]]
 hipError_t launch_combine(const void* Y, const int* k, const int* inv, const float* w,

@@ -37,30 +37,37 @@ struct NetHolder {
     static constexpr OddEvenMergeNet<NP> net{};
 };
 
-// One comparator of the network: (v, id) pairs ordered by larger logit, then lower id.
+// Sort key of a logit: the value itself, made canonical by an add of +0 (which also turns
+// -0 into +0), so that min/max compile to single v_min_f32/v_max_f32.  Non-NaN inputs.
+__device__ __forceinline__ float order_key(float f) { return f + 0.0f; }
+
+// One comparator of the network: larger value to the lower position (v_max_f32/v_min_f32).
 template <int NP, int Q>
-__device__ __forceinline__ void compare_exchange(float* v, int* id) {
+__device__ __forceinline__ void compare_exchange(float* key) {
     constexpr int a = NetHolder<NP>::net.a[Q];
     constexpr int b = NetHolder<NP>::net.b[Q];
-    const bool sw = (v[b] > v[a]) || (v[b] == v[a] && id[b] < id[a]);
-    const float va = sw ? v[b] : v[a];
-    const float vb = sw ? v[a] : v[b];
-    const int ia = sw ? id[b] : id[a];
-    const int ib = sw ? id[a] : id[b];
-    v[a] = va;
-    v[b] = vb;
-    id[a] = ia;
-    id[b] = ib;
+    const float hi = fmaxf(key[a], key[b]);
+    const float lo = fminf(key[a], key[b]);
+    key[a] = hi;
+    key[b] = lo;
 }
 
 // The whole network as straight-line code (a fold over the comparator indices), so every
 // register index is a compile-time constant regardless of loop-unrolling heuristics.
 template <int NP, int... Q>
-__device__ __forceinline__ void sort_desc(float* v, int* id, std::integer_sequence<int, Q...>) {
-    (compare_exchange<NP, Q>(v, id), ...);
+__device__ __forceinline__ void sort_desc(float* key, std::integer_sequence<int, Q...>) {
+    (compare_exchange<NP, Q>(key), ...);
 }
 
-template <int NP>
+// lowest set bit of a 64-bit mask held as two 32-bit halves (0 if empty)
+__device__ __forceinline__ int lowest_bit(uint32_t lo, uint32_t hi) {
+    if (lo) return __builtin_ctz(lo);
+    if (hi) return 32 + __builtin_ctz(hi);
+    return 0;
+}
+
+// FULL: N == NP, so every "position < N" test is static; KM: a bound on K (8 or 16)
+template <int NP, bool FULL, int KMAX>
 __global__ __launch_bounds__(256) void route_kernel(const float* __restrict__ logits, int64_t T,
                                                     int N, int K, float eps, int mode,
                                                     int renorm, int vec4, XTable xt,
@@ -68,6 +75,7 @@ __global__ __launch_bounds__(256) void route_kernel(const float* __restrict__ lo
                                                     int* __restrict__ ids,
                                                     float* __restrict__ wout) {
     constexpr int LD = NP + 1;  // padded row: lane t reads word t*LD + c, banks (t + c) % 64
+    constexpr int KM = NP < KMAX ? NP : KMAX;
     __shared__ float lds[4 * kWave * LD];
     const int lane = threadIdx.x & (kWave - 1);
     const int wv = threadIdx.x >> 6;
@@ -78,7 +86,8 @@ __global__ __launch_bounds__(256) void route_kernel(const float* __restrict__ lo
 
     // ---- stage the wave's rows (contiguous in memory) through LDS, coalesced ----
     const float* src = logits + t0 * N;
-    if (N == NP && vec4) {
+    const int Nn = FULL ? NP : N;
+    if (FULL && vec4) {
         const int total4 = rows * (NP / 4);
         for (int i = lane; i < total4; i += kWave) {
             const float4 q = reinterpret_cast<const float4*>(src)[i];
@@ -99,86 +108,177 @@ __global__ __launch_bounds__(256) void route_kernel(const float* __restrict__ lo
     }
     __syncthreads();
     if (lane >= rows) return;  // no barrier follows
+    const float* row = tile + lane * LD;
 
-    // ---- load the token's logits; pads (c >= N) sort last ----
-    float v[NP];
-    int id[NP];
+    // ---- keys of the token's logits (pads are -inf and sort last) ----
+    const float kNegInf = -INFINITY;
+    float key[NP], okey[NP];
 #pragma unroll
     for (int c = 0; c < NP; ++c) {
-        v[c] = (c < N) ? tile[lane * LD + c] : -INFINITY;
-        id[c] = c;
+        okey[c] = (c < Nn) ? order_key(row[c]) : kNegInf;
+        key[c] = okey[c];
     }
+    sort_desc<NP>(key, std::make_integer_sequence<int, NetHolder<NP>::net.n>{});
 
-    // ---- descending sort of (logit, id): larger logit first, then lower id ----
-    sort_desc<NP>(v, id, std::make_integer_sequence<int, NetHolder<NP>::net.n>{});
-
-    // ---- u_i = exp(l_(i) - l_(0)) in place; S = sum u; u_min = u_(N-1) ----
-    const float lmax = v[0];
+    // ---- u_i = exp(l_(i) - l_(0)) (0 for pads); S = sum u; u_min = u_(N-1) ----
+    const float lmax = key[0];
+    float u[NP];
     float S = 0.f;
-    float umin = 0.f;
 #pragma unroll
     for (int i = 0; i < NP; ++i) {
-        if (i < N) {
-            const float u = __builtin_amdgcn_exp2f((v[i] - lmax) * kLog2e);
-            v[i] = u;
-            S += u;
-            if (i == N - 1) umin = u;
-        }
+        u[i] = __builtin_amdgcn_exp2f((key[i] - lmax) * kLog2e);
+        S += u[i];
+    }
+    float umin = u[NP - 1];
+    if (!FULL) {
+#pragma unroll
+        for (int i = 0; i < NP; ++i) umin = (i == Nn - 1) ? u[i] : umin;
     }
 
     int k = K;
     if (mode == ELB_MODE_ELBOW) {
-        // scaled deviation: (1 - u_i) - x'_i * (1 - u_min + eps * S); D_0 == 0 exactly
+        // scaled deviation (1 - u_i) - x'_i (1 - u_min + eps S); D_0 == 0 exactly.  The first
+        // argmax only matters below K - 1 (beyond it k = K), so later points need only a max.
+        // Pads have x' = +inf and never win.
         const float Rp = (1.0f - umin) + eps * S;
         float best = 0.f;
         int e = 0;
+        float tail = -INFINITY;
 #pragma unroll
         for (int i = 1; i < NP; ++i) {
-            if (i < N) {
-                const float Di = fmaf(-xt.x[i], Rp, 1.0f - v[i]);
-                if (Di > best) {  // strict: the first index wins ties
-                    best = Di;
-                    e = i;
-                }
+            const float Di = fmaf(-xt.x[i], Rp, 1.0f - u[i]);
+            if (i < KM - 1) {
+                const bool head = i < K - 1;
+                const bool better = head && (Di > best);  // strict: first index wins ties
+                best = better ? Di : best;
+                e = better ? i : e;
+                tail = head ? tail : fmaxf(tail, Di);
+            } else {
+                tail = fmaxf(tail, Di);
             }
         }
-        k = e + 1 < K ? e + 1 : K;
+        k = (tail > best) ? K : e + 1;
     }
 
+    // ---- ids of the k selected experts: the k largest keys, equal keys by lower id ----
+    // tau = key of rank k-1; g = ranks < k with a key above tau; the rest of the k come
+    // from the experts whose key equals tau, lowest ids first.
+    float tau = key[0];
+    int g = 0;
+#pragma unroll
+    for (int i = 0; i < KM; ++i)
+        if (i == k - 1) tau = key[i];
+#pragma unroll
+    for (int i = 0; i < KM; ++i)
+        if (i < k && key[i] > tau) ++g;
+    // common case: exactly k experts have a key >= tau (no tie at the boundary)
+    uint32_t sel_lo = 0, sel_hi = 0;
+#pragma unroll
+    for (int c = 0; c < NP; ++c) {
+        const uint32_t bit = (c < Nn && okey[c] >= tau) ? (1u << (c & 31)) : 0u;
+        if (c < 32) sel_lo |= bit;
+        else sel_hi |= bit;
+    }
+    const bool tie = (__popc(sel_lo) + __popc(sel_hi)) != k;
+    if (__any(tie)) {  // wave-uniform slow path: ties at tau, lowest ids first
+        uint32_t eq_lo = 0, eq_hi = 0;
+        sel_lo = sel_hi = 0;
+#pragma unroll
+        for (int c = 0; c < NP; ++c) {
+            const uint32_t bit = 1u << (c & 31);
+            const bool real = c < Nn;
+            const uint32_t gt = (real && okey[c] > tau) ? bit : 0u;
+            const uint32_t eq = (real && okey[c] == tau) ? bit : 0u;
+            if (c < 32) {
+                sel_lo |= gt;
+                eq_lo |= eq;
+            } else {
+                sel_hi |= gt;
+                eq_hi |= eq;
+            }
+        }
+        for (int r = 0; r < k - g; ++r) {
+            const int b = lowest_bit(eq_lo, eq_hi);
+            if (b < 32) { sel_lo |= 1u << b; eq_lo &= ~(1u << b); }
+            else { sel_hi |= 1u << (b - 32); eq_hi &= ~(1u << (b - 32)); }
+        }
+    }
+    // the selected experts in id order, with their keys (re-read from the staged row)
+    int cid[KM];
+    float ck[KM];
+#pragma unroll
+    for (int r = 0; r < KM; ++r) {
+        const int b = lowest_bit(sel_lo, sel_hi);
+        const bool on = r < k;
+        cid[r] = b;
+        ck[r] = on ? order_key(row[b]) : -INFINITY;
+        if (b < 32) sel_lo &= sel_lo - 1;
+        else sel_hi &= sel_hi - 1;
+    }
+    // rank of each in descending order (equal keys: lower id, i.e. lower r, first)
+    const int64_t t = t0 + lane;
     float denom = S;
     if (renorm) {
         float sel = 0.f;
 #pragma unroll
-        for (int j = 0; j < ELB_MAX_K && j < NP; ++j)
-            if (j < k) sel += v[j];
+        for (int j = 0; j < KM; ++j)
+            if (j < k) sel += u[j];
         denom = sel;
     }
     const float inv = 1.0f / denom;
-    const int64_t t = t0 + lane;
     kout[t] = k;
 #pragma unroll
-    for (int j = 0; j < ELB_MAX_K && j < NP; ++j) {
-        if (j < K) {
-            const bool on = j < k;
-            ids[t * K + j] = on ? id[j] : -1;
-            wout[t * K + j] = on ? v[j] * inv : 0.f;
+    for (int r = 0; r < KM; ++r) {
+        if (r < k) {
+            int rank = 0;
+#pragma unroll
+            for (int q = 0; q < KM; ++q) {
+                if (q < r) rank += (q < k && ck[q] >= ck[r]) ? 1 : 0;
+                if (q > r) rank += (q < k && ck[q] > ck[r]) ? 1 : 0;
+            }
+            ids[t * K + rank] = cid[r];
+            wout[t * K + rank] =
+                __builtin_amdgcn_exp2f((ck[r] - lmax) * kLog2e) * inv;
+        }
+    }
+#pragma unroll
+    for (int j = 0; j < KM; ++j) {
+        if (j >= k && j < K) {
+            ids[t * K + j] = -1;
+            wout[t * K + j] = 0.f;
         }
     }
 }
 
-template <int NP>
+template <int NP, bool FULL, int KMAX>
 hipError_t launch_np(const float* logits, int64_t T, int N, const elb_route_params& p, int* k,
                      int* ids, float* w, hipStream_t s) {
     XTable xt;
     for (int i = 0; i < ELB_MAX_EXPERTS; ++i)
-        xt.x[i] = (i < N) ? (float)((double)i / (double)(N - 1)) : 0.f;
+        xt.x[i] = (i < N) ? (float)((double)i / (double)(N - 1)) : INFINITY;
     const int64_t waves = (T + kWave - 1) / kWave;
     const unsigned blocks = (unsigned)((waves + 3) / 4);
     const int vec4 = ((uintptr_t)logits % 16) == 0;
     ProfileScope prof("route", s);
-    hipLaunchKernelGGL(route_kernel<NP>, dim3(blocks), dim3(256), 0, s, logits, T, N, p.K,
+    hipLaunchKernelGGL((route_kernel<NP, FULL, KMAX>), dim3(blocks), dim3(256), 0, s, logits, T, N, p.K,
                        p.eps, p.mode, p.renormalize, vec4, xt, k, ids, w);
     return hipGetLastError();
+}
+
+template <int KMAX>
+hipError_t launch_k(const float* logits, int64_t T, int N, const elb_route_params& p, int* k,
+                   int* ids, float* w, hipStream_t s) {
+    switch (N) {
+        case 8: return launch_np<8, true, KMAX>(logits, T, N, p, k, ids, w, s);
+        case 16: return launch_np<16, true, KMAX>(logits, T, N, p, k, ids, w, s);
+        case 32: return launch_np<32, true, KMAX>(logits, T, N, p, k, ids, w, s);
+        case 64: return launch_np<64, true, KMAX>(logits, T, N, p, k, ids, w, s);
+        default: break;
+    }
+    if (N < 8) return launch_np<8, false, KMAX>(logits, T, N, p, k, ids, w, s);
+    if (N < 16) return launch_np<16, false, KMAX>(logits, T, N, p, k, ids, w, s);
+    if (N < 32) return launch_np<32, false, KMAX>(logits, T, N, p, k, ids, w, s);
+    return launch_np<64, false, KMAX>(logits, T, N, p, k, ids, w, s);
 }
 
 }  // namespace
@@ -186,10 +286,8 @@ hipError_t launch_np(const float* logits, int64_t T, int N, const elb_route_para
 hipError_t launch_route(const float* logits, int64_t T, int N, const elb_route_params& p,
                         int* k, int* ids, float* w, hipStream_t s) {
     if (T == 0) return hipSuccess;
-    if (N <= 8) return launch_np<8>(logits, T, N, p, k, ids, w, s);
-    if (N <= 16) return launch_np<16>(logits, T, N, p, k, ids, w, s);
-    if (N <= 32) return launch_np<32>(logits, T, N, p, k, ids, w, s);
-    return launch_np<64>(logits, T, N, p, k, ids, w, s);
+    if (p.K <= 8) return launch_k<8>(logits, T, N, p, k, ids, w, s);
+    return launch_k<ELB_MAX_K>(logits, T, N, p, k, ids, w, s);
 }
 
 }  // namespace elb
