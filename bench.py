@@ -42,16 +42,21 @@ def sha1(path):
 
 
 def time_layer(B, torch, args_gpu, K, mode, steps, warmup, profile):
+    """Average ms per whole-layer call over `steps` calls (after `warmup`), and the average
+    duration of each kernel from the library's per-launch hipEvents when `profile`."""
     x, Wr, Wgu, Wd = args_gpu
     out = torch.empty_like(x)
-    for _ in range(warmup):
+
+    def step():
         B.elb_moe_forward(x, Wr, Wgu, Wd, K=K, mode=mode, out=out)
+    for _ in range(warmup):
+        step()
     torch.cuda.synchronize()
     B.elb_profile_read()
     B.elb_profile_enable(profile)
     t0 = time.perf_counter()
     for _ in range(steps):
-        B.elb_moe_forward(x, Wr, Wgu, Wd, K=K, mode=mode, out=out)
+        step()
     torch.cuda.synchronize()
     dt = time.perf_counter() - t0
     B.elb_profile_enable(False)
@@ -93,6 +98,60 @@ def routing_only(B, torch, T=65536, N=64, K=8, nbuf=32, iters=64):
             "peak": PEAK_HBM_GBS, "frac": round(gbs / PEAK_HBM_GBS, 4)}
 
 
+GATE_UP_KERNEL = "gemm_bf16_dma<0>"    # device function behind "gemm_gate_up_bf16"
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gemm_gate_up_bf16_olmoe_prefill_traffic.json")
+GEMM_SRC = os.path.join(ROOT, "paper_2608_04401_amd", "csrc", "gemm.hip")
+COPY_BYTES = 1 << 30
+
+
+def counters_pass(B, torch, gpu, K, steps):
+    """Workload for the HBM-traffic counter runs: one plain device copy of COPY_BYTES (the
+    calibration of FETCH_SIZE / WRITE_SIZE), then `steps` whole-layer calls."""
+    a = torch.ones(COPY_BYTES // 4, dtype=torch.float32, device="cuda")
+    b = torch.empty_like(a)
+    torch.cuda.synchronize()
+    b.copy_(a)
+    torch.cuda.synchronize()
+    del a, b
+    x, Wr, Wgu, Wd = gpu
+    for _ in range(steps):
+        B.elb_moe_forward(x, Wr, Wgu, Wd, K=K)
+    torch.cuda.synchronize()
+
+
+def _counter_rows(path, counter):
+    import csv
+    rows = []
+    with open(path) as f:
+        for r in csv.DictReader(f):
+            if r["Counter_Name"] == counter:
+                rows.append((r["Kernel_Name"], float(r["Counter_Value"])))
+    return rows
+
+
+def traffic_from(fetch_csv, write_csv, command):
+    """HBM bytes per launch of the gate/up GEMM from two rocprofv3 --pmc runs of
+    `bench.py --counters` (FETCH_SIZE, then WRITE_SIZE; KiB per dispatch), each scaled by
+    what the same counter reads for the plain copy of COPY_BYTES."""
+    out = {"source_sha1": sha1(GEMM_SRC), "kernel": GATE_UP_KERNEL, "command": command}
+    for key, path, counter in (("fetch", fetch_csv, "FETCH_SIZE"),
+                               ("write", write_csv, "WRITE_SIZE")):
+        rows = _counter_rows(path, counter)
+        copy = [v for n, v in rows if "copyBuffer" in n or "copy" in n.lower()]
+        copy = max(copy)                      # the 1 GiB copy is the largest copy dispatch
+        factor = COPY_BYTES / (copy * 1024.0)
+        vals = [v for n, v in rows if GATE_UP_KERNEL in n]
+        out[key] = {"copy_kib": copy, "factor": round(factor, 4), "dispatches": len(vals),
+                    "kib_per_launch_raw": round(sum(vals) / len(vals), 1),
+                    "bytes_per_launch": round(sum(vals) / len(vals) * 1024.0 * factor)}
+    out["bytes_per_launch"] = out["fetch"]["bytes_per_launch"] + out["write"]["bytes_per_launch"]
+    os.makedirs(os.path.dirname(TRAFFIC_FILE), exist_ok=True)
+    with open(TRAFFIC_FILE, "w") as f:
+        json.dump(out, f, indent=1)
+        f.write("\n")
+    return out
+
+
 def cpu_baseline(L, K, target_s=12.0):
     """The fp64 oracle on a bounded token sample of the same workload, on this host."""
     from oracle import oracle as O
@@ -122,7 +181,16 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-routing", action="store_true")
     ap.add_argument("--no-topk", action="store_true", help="skip the fixed top-K baseline")
+    ap.add_argument("--counters", action="store_true",
+                    help="run only the workload of the HBM-traffic counter runs")
+    ap.add_argument("--traffic-from", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
+                    help="write the gate/up GEMM traffic file from two rocprofv3 counter CSVs")
+    ap.add_argument("--traffic-command", default="",
+                    help="the rocprofv3 command recorded in the traffic file")
     args = ap.parse_args()
+    if args.traffic_from:
+        print(json.dumps(traffic_from(*args.traffic_from, args.traffic_command)))
+        return
     if args.gpus != 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path "
               "(--gpus %d requested)" % args.gpus, file=sys.stderr)
@@ -141,6 +209,9 @@ def main():
     L = synth.moe_layer(T, d, N, m, dtype="bf16", seed=0)
     gpu = tuple(torch.from_numpy(a).to("cuda").to(torch.bfloat16)
                 for a in (L.x, L.W_router, L.W_gu, L.W_down))
+    if args.counters:
+        counters_pass(B, torch, gpu, K, args.steps)
+        return
 
     # routing statistics of this batch (for the useful-FLOP count)
     _, dbg = B.elb_moe_forward(*gpu, K=K, debug=True)
@@ -151,26 +222,25 @@ def main():
     counts = dbg["counts"].cpu().numpy()
     counts_top = dbg_top["counts"].cpu().numpy()
 
+    # headline: the plain timed loop; then the same loop with the library's per-launch
+    # hipEvents for the per-kernel breakdown and the roofline of the dominant kernel
     log("timing elbow layer: %d warmup, %d steps" % (args.warmup, args.steps))
-    ms, kern = time_layer(B, torch, gpu, K, B.MODE_ELBOW, args.steps, args.warmup, True)
+    ms, _ = time_layer(B, torch, gpu, K, B.MODE_ELBOW, args.steps, args.warmup, False)
+    ms_ev, kern = time_layer(B, torch, gpu, K, B.MODE_ELBOW, args.steps, 2, True)
     ms_top, kern_top = None, {}
     if not args.no_topk:
         log("timing top-8 baseline")
-        ms_top, kern_top = time_layer(B, torch, gpu, K, B.MODE_TOPK, args.steps, args.warmup,
-                                      True)
-    # same timed loop without the per-kernel events, for the event overhead
-    ms_noev, _ = time_layer(B, torch, gpu, K, B.MODE_ELBOW, args.steps, 2, False)
+        ms_top, _ = time_layer(B, torch, gpu, K, B.MODE_TOPK, args.steps, args.warmup, False)
+        _, kern_top = time_layer(B, torch, gpu, K, B.MODE_TOPK, args.steps, 2, True)
 
     g1 = "gemm_gate_up_bf16"
     flop_g1 = 4.0 * d * m * sum_k            # useful FLOPs of the gate/up GEMM per launch
     us_g1 = kern[g1] * 1e3
     achieved = flop_g1 / (us_g1 * 1e-6) / 1e12
-    traffic = None
-    tfile = os.path.join(ROOT, "profiles", "gemm_gate_up_bf16_olmoe_prefill_traffic.json")
-    if os.path.exists(tfile):
-        tj = json.load(open(tfile))
-        if tj.get("source_sha1") == sha1(os.path.join(ROOT, "paper_2608_04401_amd", "csrc",
-                                                      "gemm.hip")):
+    traffic = None           # null once the kernel source differs from the one counted
+    if args.workload == "olmoe-prefill" and os.path.exists(TRAFFIC_FILE):
+        tj = json.load(open(TRAFFIC_FILE))
+        if tj.get("source_sha1") == sha1(GEMM_SRC):
             traffic = tj.get("bytes_per_launch")
     flop_all = 6.0 * d * m * sum_k
     res = {
@@ -198,7 +268,7 @@ def main():
         "expert_flop_fraction_of_peak": round(flop_all / (sum(
             kern[n] for n in kern if n.startswith("gemm")) * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
         "kernels_us": {n: round(v * 1e3, 2) for n, v in kern.items()},
-        "ms_per_step_without_kernel_events": round(ms_noev, 4),
+        "ms_per_step_with_kernel_events": round(ms_ev, 4),
         "topk_baseline": None if ms_top is None else {
             "value": round(T / (ms_top * 1e-3), 1), "unit": "tokens/s",
             "ms_per_step": round(ms_top, 4), "sum_k": sum_k_top,

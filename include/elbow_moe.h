@@ -131,7 +131,7 @@ int elb_dispatch(const int32_t *k, const int32_t *ids, int64_t T, int32_t N, int
  *   y         [T, d]      dtype   output; may alias residual, must not alias x
  *   workspace             at least elb_moe_workspace_bytes(T, d, N, m, K, dtype) bytes
  * Requirements: 2 <= N <= ELB_MAX_EXPERTS; 1 <= K <= min(N, ELB_MAX_K);
- * ELB_BF16: d % 64 == 0 and m % 64 == 0; ELB_F32: d % 4 == 0 and m % 4 == 0.
+ * ELB_BF16: d % 64 == 0 and m % 64 == 0; ELB_F32: d % 16 == 0 and m % 16 == 0.
  */
 size_t elb_moe_workspace_bytes(int64_t T, int32_t d, int32_t N, int32_t m, int32_t K,
                                int32_t dtype);

@@ -4,7 +4,7 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
-#include "../../include/elbow_moe.h"
+#include "elbow_moe.h"
 
 namespace elb {
 

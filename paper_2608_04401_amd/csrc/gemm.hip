@@ -213,149 +213,6 @@ __global__ __launch_bounds__(256) void gemm_bf16(const bf16_t* __restrict__ A,
 }
 
 // ------------------------------------------------------------------------------------------
-// bf16 MFMA kernel, large tiles: 256 x 256 x 64 block tile, 4 waves (2 x 2) of 128 x 128,
-// v_mfma_f32_32x32x16_bf16 (4 x 4 per wave, 256 fp32 accumulators per lane).  Per FLOP this
-// reads half the LDS bytes of the 64 x 64 wave tile.  LDS: 2 stages x (256 + 256) rows x 72.
-// ------------------------------------------------------------------------------------------
-constexpr int LBM = 256, LBN = 256;
-
-typedef float f32x16_t __attribute__((ext_vector_type(16)));
-
-template <int MODE>
-__global__ __launch_bounds__(256) void gemm_bf16_l(const bf16_t* __restrict__ A,
-                                                   const int* __restrict__ row_token,
-                                                   const bf16_t* __restrict__ B,
-                                                   const int* __restrict__ offsets,
-                                                   const int* __restrict__ tile_off, int N,
-                                                   int d, int m, bf16_t* __restrict__ C) {
-    __shared__ __attribute__((aligned(16))) bf16_t As[2][LBM][LDK];
-    __shared__ __attribute__((aligned(16))) bf16_t Bs[2][LBN][LDK];
-
-    const int nt_count = (MODE == 0) ? m / 128 : (d + LBN - 1) / LBN;
-    int tile, ntile;
-    if (!xcd_tile(blockIdx.x, tile_off[N] * nt_count, nt_count, tile, ntile)) return;
-    int e, row0, rows;
-    find_tile(tile_off, offsets, N, tile, LBM, e, row0, rows);
-
-    const int tid = threadIdx.x;
-    const int lane = tid & 63;
-    const int wid = tid >> 6;
-    const int wm = wid >> 1, wn = wid & 1;
-    const int Kd = (MODE == 0) ? d : m;
-
-    // loader: thread handles rows r0 + 32 i (i < 8) of both tiles, 16-byte chunk kc
-    const int r0 = tid >> 3;
-    const int kc = (tid & 7) * 8;
-    const bf16_t* a_src[8];
-    const bf16_t* b_src[8];
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-        const int r = r0 + 32 * i;
-        const int rr = r < rows ? r : rows - 1;  // rows past the expert's end: clamp, unused
-        if (MODE == 0) {
-            a_src[i] = A + (int64_t)row_token[row0 + rr] * d + kc;
-            const int hc = ntile * 128;  // first H column of this tile
-            const int brow = (r < 128) ? (hc + r) : (m + hc + (r - 128));
-            b_src[i] = B + ((int64_t)e * 2 * m + brow) * d + kc;
-        } else {
-            a_src[i] = A + (int64_t)(row0 + rr) * m + kc;
-            int brow = ntile * LBN + r;
-            brow = brow < d ? brow : d - 1;
-            b_src[i] = B + ((int64_t)e * d + brow) * m + kc;
-        }
-    }
-
-    int brow_base[4];
-#pragma unroll
-    for (int ni = 0; ni < 4; ++ni)
-        brow_base[ni] = (MODE == 0) ? ((ni < 2) ? (wn * 64 + ni * 32) : (128 + wn * 64 + (ni - 2) * 32))
-                                    : (wn * 128 + ni * 32);
-
-    f32x16_t acc[4][4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-#pragma unroll
-            for (int q = 0; q < 16; ++q) acc[i][j][q] = 0.f;
-
-    u32x4_t ra[8], rb[8];
-    const int nk = Kd / BK;
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-        ra[i] = *reinterpret_cast<const u32x4_t*>(a_src[i]);
-        rb[i] = *reinterpret_cast<const u32x4_t*>(b_src[i]);
-    }
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-        *reinterpret_cast<u32x4_t*>(&As[0][r0 + 32 * i][kc]) = ra[i];
-        *reinterpret_cast<u32x4_t*>(&Bs[0][r0 + 32 * i][kc]) = rb[i];
-    }
-    __syncthreads();
-    const int l32 = lane & 31;
-    const int kq = (lane >> 5) * 8;
-    for (int kt = 0; kt < nk; ++kt) {
-        const int buf = kt & 1;
-        const bool more = kt + 1 < nk;
-        if (more) {
-            const int k0 = (kt + 1) * BK;
-#pragma unroll
-            for (int i = 0; i < 8; ++i) {
-                ra[i] = *reinterpret_cast<const u32x4_t*>(a_src[i] + k0);
-                rb[i] = *reinterpret_cast<const u32x4_t*>(b_src[i] + k0);
-            }
-        }
-#pragma unroll
-        for (int ks = 0; ks < BK / 16; ++ks) {
-            bf16x8_t af[4], bfr[4];
-#pragma unroll
-            for (int mi = 0; mi < 4; ++mi)
-                af[mi] = *reinterpret_cast<const bf16x8_t*>(&As[buf][wm * 128 + mi * 32 + l32][ks * 16 + kq]);
-#pragma unroll
-            for (int ni = 0; ni < 4; ++ni)
-                bfr[ni] = *reinterpret_cast<const bf16x8_t*>(&Bs[buf][brow_base[ni] + l32][ks * 16 + kq]);
-#pragma unroll
-            for (int mi = 0; mi < 4; ++mi)
-#pragma unroll
-                for (int ni = 0; ni < 4; ++ni)
-                    acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[mi], bfr[ni], acc[mi][ni], 0, 0, 0);
-        }
-        if (more) {
-#pragma unroll
-            for (int i = 0; i < 8; ++i) {
-                *reinterpret_cast<u32x4_t*>(&As[buf ^ 1][r0 + 32 * i][kc]) = ra[i];
-                *reinterpret_cast<u32x4_t*>(&Bs[buf ^ 1][r0 + 32 * i][kc]) = rb[i];
-            }
-        }
-        __syncthreads();
-    }
-
-    // epilogue: accumulator q of a 32 x 32 fragment is row (q/4)*8 + (lane/32)*4 + q%4,
-    // column lane%32
-    const int rq = (lane >> 5) * 4;
-#pragma unroll
-    for (int mi = 0; mi < 4; ++mi)
-#pragma unroll
-        for (int q = 0; q < 16; ++q) {
-            const int lr = wm * 128 + mi * 32 + (q >> 2) * 8 + rq + (q & 3);
-            if (lr >= rows) continue;
-            if (MODE == 0) {
-                bf16_t* dst = C + (int64_t)(row0 + lr) * m + ntile * 128 + wn * 64 + l32;
-#pragma unroll
-                for (int ni = 0; ni < 2; ++ni)
-                    dst[ni * 32] = f32_to_bf16(silu(acc[mi][ni][q]) * acc[mi][ni + 2][q]);
-            } else {
-                bf16_t* dst = C + (int64_t)(row0 + lr) * d;
-#pragma unroll
-                for (int ni = 0; ni < 4; ++ni) {
-                    const int col = ntile * LBN + wn * 128 + ni * 32 + l32;
-                    if (col < d) dst[col] = f32_to_bf16(acc[mi][ni][q]);
-                }
-            }
-        }
-}
-
-// ------------------------------------------------------------------------------------------
 // bf16 MFMA kernel with LDS DMA and a 4-stage pipeline: 256 x 256 block tile, k-tiles of 32,
 // 4 waves (2 x 2) of 128 x 128, v_mfma_f32_32x32x16_bf16.  Tiles are copied global -> LDS by
 // global_load_lds_dwordx4 (no staging registers, no ds_write), three k-tiles ahead of the one
@@ -363,6 +220,9 @@ __global__ __launch_bounds__(256) void gemm_bf16_l(const bf16_t* __restrict__ A,
 // are unpadded (64 B) with their four 16-byte chunks XOR-swizzled per row so that the 16 lanes
 // of one ds_read_b128 pass (16 consecutive rows, same logical chunk) hit distinct banks.
 // ------------------------------------------------------------------------------------------
+constexpr int LBM = 256, LBN = 256;
+
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
 typedef __attribute__((address_space(3))) void lds_void_t;
 typedef __attribute__((address_space(1))) void glb_void_t;
 
