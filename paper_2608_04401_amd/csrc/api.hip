@@ -257,7 +257,7 @@ static int experts_impl(const void* x, const void* W_gate_up, const void* W_down
     int* inv = (int*)(ws + L.inv);
     void* H = ws + L.H;
     void* Y = ws + L.Y;
-    const int tr = gemm_tile_rows(dtype, T, K, N, m);
+    const int tr = gemm_tile_rows(dtype, T, K, N, d, m);
     const int64_t mt = max_tiles(T, K, N, tr);
     if (int rc = hip_status(launch_dispatch(k, ids, T, N, K, counts, offsets, row_token, inv,
                                             hist, tile_off, tr, s), "dispatch"))

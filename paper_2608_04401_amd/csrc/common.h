@@ -47,7 +47,7 @@ hipError_t launch_router(const void* x, const void* Wr, int64_t T, int d, int N,
 
 // grouped GEMMs
 // rows per M-tile of the grouped GEMMs for this problem (the dispatch scan uses the same)
-int gemm_tile_rows(int dtype, int64_t T, int K, int N, int m);
+int gemm_tile_rows(int dtype, int64_t T, int K, int N, int d, int m);
 hipError_t launch_gemm_gate_up(const void* x, const void* Wgu, const int* row_token,
                                const int* offsets, const int* tile_off, int64_t max_tiles,
                                int tile_rows, int d, int N, int m, int dtype, void* H,

@@ -213,39 +213,60 @@ __global__ __launch_bounds__(256) void gemm_bf16(const bf16_t* __restrict__ A,
 }
 
 // ------------------------------------------------------------------------------------------
-// bf16 MFMA kernel with LDS DMA and a 4-stage pipeline: 256 x 256 block tile, k-tiles of 32,
-// 4 waves (2 x 2) of 128 x 128, v_mfma_f32_32x32x16_bf16.  Tiles are copied global -> LDS by
-// global_load_lds_dwordx4 (no staging registers, no ds_write), three k-tiles ahead of the one
-// being multiplied, so the copy latency is covered by three k-tiles of MFMA work.  LDS rows
-// are unpadded (64 B) with their four 16-byte chunks XOR-swizzled per row so that the 16 lanes
-// of one ds_read_b128 pass (16 consecutive rows, same logical chunk) hit distinct banks.
+// bf16 MFMA kernel with LDS DMA: 256 x 256 block tile, k-tiles of 64, 4 waves (2 x 2) of
+// 128 x 128, v_mfma_f32_32x32x16_bf16, one block per CU (the copy ring takes all 160 KB of LDS).
+//
+// Copies: global_load_lds_dwordx4 (no staging registers, no ds_write).  Each copy
+// instruction moves 8 rows x 128 bytes, one whole cache line per row: the copy rate is bound
+// by the misses a CU's vector cache can keep in flight, so full lines move twice the bytes
+// per miss of half lines.  The A half (token rows) and the B half (weight rows) of a k-tile
+// are separate 32 KB units of a 5-unit ring; the B half, which usually misses to HBM, is
+// issued two k-tiles ahead of its use and the A half one k-tile ahead.  LDS rows are
+// unpadded (128 B) with their eight 16-byte chunks XOR-swizzled per row so that the 16
+// lanes of one ds_read_b128 pass (16 consecutive rows, same logical chunk) hit distinct banks.
+//
+// MFMA operands are swapped (weights as the first operand): each accumulator tile is then the
+// transpose of the output tile, so a lane holds 4 consecutive output columns of one token row
+// per group of 4 registers.  The epilogue writes them (bf16, 8 bytes per lane) into a padded
+// row-major tile in LDS and the block then stores whole rows with 16-byte coalesced stores.
 // ------------------------------------------------------------------------------------------
 constexpr int LBM = 256, LBN = 256;
 
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
+typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
 typedef __attribute__((address_space(3))) void lds_void_t;
-typedef __attribute__((address_space(1))) void glb_void_t;
 
-// physical 16-byte chunk of logical chunk c (0..3) in LDS row r
-__device__ __forceinline__ int swz(int r, int c) {
-    return c ^ (((r >> 2) & 1) | ((((r >> 1) ^ (r >> 3)) & 1) << 1));
+// physical 16-byte chunk of logical chunk c (0..7) in a 128-byte LDS row r
+__device__ __forceinline__ int swz8(int r, int c) {
+    return c ^ (((r >> 1) ^ ((r & 1) << 2)) & 7);
 }
 
 // s_waitcnt vmcnt(n) (expcnt and lgkmcnt not waited on)
 #define ELB_WAIT_VMCNT(n) __builtin_amdgcn_s_waitcnt(((n) & 15) | (((n) >> 4) << 14) | 0x0F70)
 
+// two floats -> two bf16 (round to nearest even) in one v_cvt_pk_bf16_f32
+typedef __bf16 bf16x2_vt __attribute__((ext_vector_type(2)));
+typedef float f32x2_vt __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+    const f32x2_vt v = {lo, hi};
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2_vt));
+}
+
 template <int MODE>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) void gemm_bf16_dma(const bf16_t* __restrict__ A,
-                                                     const int* __restrict__ row_token,
-                                                     const bf16_t* __restrict__ B,
-                                                     const int* __restrict__ offsets,
-                                                     const int* __restrict__ tile_off, int N,
-                                                     int d, int m, bf16_t* __restrict__ C) {
-    constexpr int TM = 256, TN = 256, TK = 32;
-    // one array per pipeline stage, so that the compiler sees which stage each LDS access
-    // and each copy touches
-    __shared__ __attribute__((aligned(1024))) bf16_t As0[TM * TK], As1[TM * TK], As2[TM * TK], As3[TM * TK];
-    __shared__ __attribute__((aligned(1024))) bf16_t Bs0[TN * TK], Bs1[TN * TK], Bs2[TN * TK], Bs3[TN * TK];
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) void gemm_bf16_dma(
+    const bf16_t* __restrict__ A, const int* __restrict__ row_token,
+    const bf16_t* __restrict__ B, const int* __restrict__ offsets,
+    const int* __restrict__ tile_off, int N, int d, int m, bf16_t* __restrict__ C) {
+    constexpr int TM = 256, TN = 256, TK = 64;
+    constexpr int UNIT = TM * TK;  // elements of one ring unit: the A or the B half of a k-tile
+    constexpr int NU = 5;          // units in the ring
+    constexpr int OUTC = (MODE == 0) ? 128 : TN;  // output columns of the block
+    constexpr int PITCH = OUTC * 2 + 16;          // bytes per row of the staged output tile
+    static_assert(TM == TN && TM * PITCH <= NU * UNIT * 2, "staging tile exceeds LDS");
+    // One array: its address is passed to the copy instructions (inline assembly), which tells
+    // the compiler that all of it may be written there.
+    __shared__ __attribute__((aligned(1024))) char sm_bytes[NU * UNIT * 2];
+    bf16_t* const sm = reinterpret_cast<bf16_t*>(sm_bytes);
 
     const int nt_count = (MODE == 0) ? m / 128 : (d + TN - 1) / TN;
     int tile, ntile;
@@ -259,14 +280,14 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
     const int wm = wid >> 1, wn = wid & 1;
     const int Kd = (MODE == 0) ? d : m;
 
-    // DMA sources: wave w copies rows [64w, 64w + 64) of each tile, 16 rows (1 KB) per
-    // instruction; lane l fills physical chunk l & 3 of row 64w + 16i + (l >> 2), so it
-    // fetches that row's logical chunk swz(row, l & 3) (the XOR is its own inverse).
-    uint32_t a_off[4], b_off[4];  // element offsets of each row's chunk (k = 0)
+    // Copy sources: wave w copies rows [64w, 64w + 64) of each tile, 8 rows (1 KB) per
+    // instruction; lane l fills physical chunk l & 7 of row 64w + 8i + (l >> 3), so it
+    // fetches that row's logical chunk swz8(row, l & 7) (the XOR is its own inverse).
+    uint32_t a_off[8], b_off[8];  // element offsets of each row's chunk (k = 0)
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        const int r = 64 * wid + 16 * i + (lane >> 2);
-        const int c = swz(r, lane & 3);
+    for (int i = 0; i < 8; ++i) {
+        const int r = 64 * wid + 8 * i + (lane >> 3);
+        const int c = swz8(r, lane & 7);
         const int rr = r < rows ? r : rows - 1;  // rows past the expert's end: clamp, unused
         if (MODE == 0) {
             a_off[i] = (uint32_t)row_token[row0 + rr] * (uint32_t)d + c * 8;
@@ -280,28 +301,25 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
             b_off[i] = ((uint32_t)e * (uint32_t)d + brow) * (uint32_t)m + c * 8;
         }
     }
-    // The copies are issued with inline assembly: the compiler cannot tell which LDS stage a
-    // copy writes, and would otherwise wait for every copy in flight before each LDS read.
-    // Waits are explicit below (ELB_WAIT_VMCNT); M0 carries the wave's LDS destination and is
-    // set in the same statement.
-    auto issue = [&](bf16_t* as, bf16_t* bs, int k0) {
+    // LDS byte address of this wave's first 8-row group in unit 0
+    const uint32_t lds0 = (uint32_t)(uintptr_t)(lds_void_t*)sm_bytes +
+                          (uint32_t)__builtin_amdgcn_readfirstlane(wid * 64 * TK * 2);
+    // The copies are inline assembly: the compiler cannot tell which unit a copy writes, and
+    // would otherwise wait for every copy in flight before each LDS read.  Waits are explicit
+    // (ELB_WAIT_VMCNT); M0 carries the LDS destination and is set in the same statement.
+    // Each call is 8 copy instructions per wave.
+    auto issue = [&](const bf16_t* src, const uint32_t (&off)[8], int unit, int k0) {
+        const uint32_t base = lds0 + (uint32_t)unit * (UNIT * 2);
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const uint32_t la = __builtin_amdgcn_readfirstlane(
-                (uint32_t)(uintptr_t)(lds_void_t*)(as + (64 * wid + 16 * i) * TK));
-            const uint32_t lb = __builtin_amdgcn_readfirstlane(
-                (uint32_t)(uintptr_t)(lds_void_t*)(bs + (64 * wid + 16 * i) * TK));
-            const uint32_t va = (a_off[i] + k0) * 2u;  // byte offsets
-            const uint32_t vb = (b_off[i] + k0) * 2u;
+        for (int i = 0; i < 8; ++i) {
+            const uint32_t la = base + i * 1024;
+            const uint32_t va = (off[i] + k0) * 2u;  // byte offset
             asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2"
-                         :: "s"(la), "v"(va), "s"(A) : "memory", "m0");
-            asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2"
-                         :: "s"(lb), "v"(vb), "s"(B) : "memory", "m0");
+                         :: "s"(la), "v"(va), "s"(src) : "memory", "m0");
         }
     };
 
-    // fragment addresses (element offsets inside a stage); the swizzle of a fragment row
-    // depends on its row mod 16, which is l32 mod 16
+    // fragment rows (element offsets inside a stage)
     const int l32 = lane & 31;
     const int hi = lane >> 5;
     int a_frag[4], b_frag[4];
@@ -313,7 +331,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
                                    : (wn * 128 + ni * 32);
         b_frag[ni] = (br + l32) * TK;
     }
-    const int c0 = swz(l32, hi) * 8, c1 = swz(l32, 2 + hi) * 8;
+    // element offset of the chunk this lane reads for k16-step kk (k = 16 kk .. 16 kk + 15);
+    // fragment rows are l32 mod 16 modulo 16, so the swizzle depends on l32 only
+    int cofs[4];
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk) cofs[kk] = swz8(l32, 2 * kk + hi) * 8;
 
     f32x16_t acc[4][4];
 #pragma unroll
@@ -323,81 +345,136 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
 #pragma unroll
             for (int q = 0; q < 16; ++q) acc[i][j][q] = 0.f;
 
-    auto consume = [&](const bf16_t* as, const bf16_t* bs) {
-        bf16x8_t a0[4], b0[4], a1[4], b1[4];
+    // Two fragment register sets: the 8 LDS reads of the next k16-step are issued between
+    // the first 8 of the 16 MFMAs of the current one, which run on the other set.
+    bf16x8_t fa0[4], fb0[4], fa1[4], fb1[4];
+    auto load = [&](bf16x8_t (&fa)[4], bf16x8_t (&fb)[4], int ua, int ub, int kk) {
+        const bf16_t* sa = sm + ua * UNIT + cofs[kk];
+        const bf16_t* sb = sm + ub * UNIT + cofs[kk];
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-            a0[i] = *reinterpret_cast<const bf16x8_t*>(as + a_frag[i] + c0);
-            b0[i] = *reinterpret_cast<const bf16x8_t*>(bs + b_frag[i] + c0);
+            fa[i] = *reinterpret_cast<const bf16x8_t*>(sa + a_frag[i]);
+            fb[i] = *reinterpret_cast<const bf16x8_t*>(sb + b_frag[i]);
         }
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            a1[i] = *reinterpret_cast<const bf16x8_t*>(as + a_frag[i] + c1);
-            b1[i] = *reinterpret_cast<const bf16x8_t*>(bs + b_frag[i] + c1);
-        }
+    };
+    auto mma = [&](const bf16x8_t (&fa)[4], const bf16x8_t (&fb)[4], bool reads) {
 #pragma unroll
         for (int mi = 0; mi < 4; ++mi)
 #pragma unroll
             for (int ni = 0; ni < 4; ++ni)
-                acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0[mi], b0[ni], acc[mi][ni], 0, 0, 0);
+                acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[ni], fa[mi], acc[mi][ni], 0, 0, 0);
+        if (reads) {
 #pragma unroll
-        for (int mi = 0; mi < 4; ++mi)
-#pragma unroll
-            for (int ni = 0; ni < 4; ++ni)
-                acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1[mi], b1[ni], acc[mi][ni], 0, 0, 0);
+            for (int i = 0; i < 8; ++i) {
+                __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // one LDS read
+                __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
+            }
+            __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
+        }
     };
 
-    // Stage j of k-tile kt is consumed after waiting for its copy: each issue() is 8 copy
-    // instructions per wave and copies complete in order, so with s later stages already
-    // issued the wave waits for vmcnt <= 8 s; the barrier then makes every wave's part
-    // visible and guarantees that the stage about to be refilled is no longer being read.
-    const int nk = Kd / TK;  // a multiple of 4 (Kd % 128 == 0 for this kernel)
-    issue(As0, Bs0, 0);
-    issue(As1, Bs1, TK);
-    issue(As2, Bs2, 2 * TK);
-    // A bare s_barrier, not __syncthreads(): the latter's workgroup fence would make the
-    // compiler drain every copy in flight (vmcnt(0)) and collapse the pipeline.  Visibility
-    // is explicit instead: each wave waits for its own copies of stage J, and every LDS read
-    // of the stage being refilled has completed (its MFMAs consumed it) before the barrier.
-#define ELB_STEP(J, AJ, BJ, AP, BP)                                   \
-    {                                                                 \
-        const int kj = kt + (J);                                      \
-        if (kj + 2 < nk) ELB_WAIT_VMCNT(16);                          \
-        else if (kj + 1 < nk) ELB_WAIT_VMCNT(8);                      \
-        else ELB_WAIT_VMCNT(0);                                       \
-        __builtin_amdgcn_s_barrier();                                 \
-        if (kj + 3 < nk) issue(AP, BP, (kj + 3) * TK);                \
-        consume(AJ, BJ);                                              \
-    }
-    for (int kt = 0; kt < nk; kt += 4) {
-        ELB_STEP(0, As0, Bs0, As3, Bs3)
-        ELB_STEP(1, As1, Bs1, As0, Bs0)
-        ELB_STEP(2, As2, Bs2, As1, Bs1)
-        ELB_STEP(3, As3, Bs3, As2, Bs2)
-    }
-#undef ELB_STEP
-
-    const int rq = hi * 4;
-#pragma unroll
-    for (int mi = 0; mi < 4; ++mi)
-#pragma unroll
-        for (int q = 0; q < 16; ++q) {
-            const int lr = wm * 128 + mi * 32 + (q >> 2) * 8 + rq + (q & 3);
-            if (lr >= rows) continue;
-            if (MODE == 0) {
-                bf16_t* dst = C + (int64_t)(row0 + lr) * m + ntile * 128 + wn * 64 + l32;
-#pragma unroll
-                for (int ni = 0; ni < 2; ++ni)
-                    dst[ni * 32] = f32_to_bf16(silu(acc[mi][ni][q]) * acc[mi][ni + 2][q]);
-            } else {
-                bf16_t* dst = C + (int64_t)(row0 + lr) * d;
-#pragma unroll
-                for (int ni = 0; ni < 4; ++ni) {
-                    const int col = ntile * TN + wn * 128 + ni * 32 + l32;
-                    if (col < d) dst[col] = f32_to_bf16(acc[mi][ni][q]);
-                }
-            }
+    // Pipeline: the B half of k-tile t lives in unit 2t mod 5, its A half in unit 2t + 1
+    // mod 5.  After the third k16-step of tile t each wave waits for its own copies of tile
+    // t + 1 and for its own LDS reads; the barrier then makes tile t + 1 visible to every wave
+    // and frees tile t's two units (every read of them has completed), which receive the A
+    // half of tile t + 2 and the B half of tile t + 3 before the fourth k16-step runs.  Copies
+    // complete in order and each half is 8 instructions per wave; the only copies issued after
+    // tile t + 1's are those of B(t + 2), so the wait is vmcnt <= 8 (0 near the end).
+    // A bare s_barrier, not __syncthreads(): the latter's fence would make the compiler drain
+    // every copy in flight.
+    const int nk = Kd / TK;  // >= 1
+    // as if barriers at t = -3, -2, -1 had issued B(0); A(0), B(1); A(1), B(2)
+    issue(B, b_off, 0, 0);
+    issue(A, a_off, 1, 0);
+    if (nk > 1) {
+        issue(B, b_off, 2, TK);
+        issue(A, a_off, 3, TK);
+        if (nk > 2) {
+            issue(B, b_off, 4, 2 * TK);
+            ELB_WAIT_VMCNT(24);
+        } else {
+            ELB_WAIT_VMCNT(16);
         }
+    } else {
+        ELB_WAIT_VMCNT(0);
+    }
+    __builtin_amdgcn_s_barrier();
+    int ub = 0, ua = 1;  // units of tile t
+    load(fa0, fb0, ua, ub, 0);
+    int t = 0;
+    for (; t < nk - 1; ++t) {
+        const int ub1 = ub + 2 >= NU ? ub + 2 - NU : ub + 2;  // units of tile t + 1
+        const int ua1 = ua + 2 >= NU ? ua + 2 - NU : ua + 2;
+        load(fa1, fb1, ua, ub, 1);
+        mma(fa0, fb0, true);
+        load(fa0, fb0, ua, ub, 2);
+        mma(fa1, fb1, true);
+        load(fa1, fb1, ua, ub, 3);
+        mma(fa0, fb0, true);
+        __builtin_amdgcn_sched_barrier(0);
+        if (t + 2 < nk) ELB_WAIT_VMCNT(8);
+        else ELB_WAIT_VMCNT(0);
+        asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+        if (t + 2 < nk) issue(A, a_off, ub, (t + 2) * TK);   // A(t + 2) -> unit 2t
+        if (t + 3 < nk) issue(B, b_off, ua, (t + 3) * TK);   // B(t + 3) -> unit 2t + 1
+        __builtin_amdgcn_sched_barrier(0);
+        load(fa0, fb0, ua1, ub1, 0);
+        mma(fa1, fb1, true);
+        ub = ub1;
+        ua = ua1;
+    }
+    {   // last k-tile
+        load(fa1, fb1, ua, ub, 1);
+        mma(fa0, fb0, true);
+        load(fa0, fb0, ua, ub, 2);
+        mma(fa1, fb1, true);
+        load(fa1, fb1, ua, ub, 3);
+        mma(fa0, fb0, true);
+        mma(fa1, fb1, false);
+    }
+
+    // Epilogue through LDS: every wave is past its last LDS read of the stages.
+    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+    char* const stg = sm_bytes;
+#pragma unroll
+    for (int mi = 0; mi < 4; ++mi) {
+        char* const rowp = stg + (wm * 128 + mi * 32 + l32) * PITCH + hi * 8;
+#pragma unroll
+        for (int ni = 0; ni < ((MODE == 0) ? 2 : 4); ++ni)
+#pragma unroll
+            for (int g = 0; g < 4; ++g) {
+                float v[4];
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const float a0 = acc[mi][ni][4 * g + r];
+                    v[r] = (MODE == 0) ? silu(a0) * acc[mi][ni + 2][4 * g + r] : a0;
+                }
+                const int col = ((MODE == 0) ? wn * 64 : wn * 128) + ni * 32 + g * 8;
+                u32x2_t pk = {pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
+                *reinterpret_cast<u32x2_t*>(rowp + col * 2) = pk;
+            }
+    }
+    __syncthreads();
+    // each thread stores one fixed 16-byte column chunk of every RPI-th row
+    constexpr int CPR = OUTC * 2 / 16;  // 16-byte chunks per row
+    constexpr int RPI = 256 / CPR;      // rows per pass of the block
+    const int cc = tid % CPR, r0 = tid / CPR;
+    const int ldc = (MODE == 0) ? m : d;
+    const int col = ntile * OUTC + cc * 8;
+    const bool col_ok = (MODE == 0) || col < d;
+    const char* src = stg + r0 * PITCH + cc * 16;
+    bf16_t* dst = C + (int64_t)(row0 + r0) * ldc + col;
+#pragma unroll
+    for (int b = 0; b < TM / RPI; b += 16) {
+        u32x4_t v[16];
+#pragma unroll
+        for (int i = 0; i < 16; ++i)
+            v[i] = *reinterpret_cast<const u32x4_t*>(src + (b + i) * RPI * PITCH);
+#pragma unroll
+        for (int i = 0; i < 16; ++i)
+            if (col_ok && r0 + (b + i) * RPI < rows)
+                *reinterpret_cast<u32x4_t*>(dst + (int64_t)(b + i) * RPI * ldc) = v[i];
+    }
 }
 
 // ------------------------------------------------------------------------------------------
@@ -497,10 +574,10 @@ unsigned grid8(int64_t blocks) { return (unsigned)((blocks + 7) / 8 * 8); }
 
 }  // namespace
 
-int gemm_tile_rows(int dtype, int64_t T, int K, int N, int m) {
+int gemm_tile_rows(int dtype, int64_t T, int K, int N, int d, int m) {
     if (dtype != ELB_BF16) return FBM;
     const int64_t avg_rows = T * K / (N > 0 ? N : 1);
-    return (m % 128 == 0 && T > 0 && avg_rows >= 192) ? LBM : BM;
+    return (m % 128 == 0 && d >= 128 && T > 0 && avg_rows >= 192) ? LBM : BM;
 }
 
 hipError_t launch_gemm_gate_up(const void* x, const void* Wgu, const int* row_token,

@@ -111,6 +111,17 @@ def test_experts_bf16_ragged_with_residual():
     _experts_case(L, BF, 4, O.MODE_ELBOW, RTOL_BF16, residual=res)
 
 
+@pytest.mark.parametrize("T,d,N,m,K", [(1000, 192, 8, 128, 2), (1536, 320, 4, 256, 2)])
+def test_experts_bf16_large_tiles_ragged(T, d, N, m, K):
+    """Shapes on the 256-row tile path (>= 192 rows per expert on average) with a partial
+    output tile in the down GEMM (d not a multiple of 256) and few k-tiles (d = 192: 3 in
+    the gate/up GEMM; m = 128: 2 in the down GEMM), with a residual."""
+    L = synth.moe_layer(T, d, N, m, dtype="bf16", seed=T + d)
+    res = synth.round_bf16(synth.gaussian_logits(T, d, seed=7))
+    _experts_case(L, BF, K, O.MODE_ELBOW, RTOL_BF16, residual=res)
+    _experts_case(L, BF, K, O.MODE_TOPK, RTOL_BF16)
+
+
 @pytest.mark.parametrize("mode", [O.MODE_ELBOW, O.MODE_TOPK])
 def test_experts_bf16_olmoe_sampled(olmoe, mode):
     L = olmoe[0]
