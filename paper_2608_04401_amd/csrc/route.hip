@@ -84,20 +84,29 @@ __global__ __launch_bounds__(256) void route_kernel(const float* __restrict__ lo
     int rows = 0;
     if (t0 < T) rows = (int)((T - t0) < kWave ? (T - t0) : kWave);
 
-    // ---- stage the wave's rows (contiguous in memory) through LDS, coalesced ----
+    // ---- stage the wave's rows (contiguous in memory) through LDS, coalesced: every load
+    // of the lane is issued before the first LDS write, so the wave waits for memory once ----
     const float* src = logits + t0 * N;
     const int Nn = FULL ? NP : N;
     if (FULL && vec4) {
+        constexpr int PER = NP / 4;  // float4 per lane (64 rows x NP / 4 per wave)
         const int total4 = rows * (NP / 4);
-        for (int i = lane; i < total4; i += kWave) {
-            const float4 q = reinterpret_cast<const float4*>(src)[i];
+        float4 q[PER];
+#pragma unroll
+        for (int it = 0; it < PER; ++it) {
+            const int i = lane + it * kWave;
+            if (rows == kWave || i < total4) q[it] = reinterpret_cast<const float4*>(src)[i];
+        }
+        __builtin_amdgcn_sched_barrier(0);  // keep every load ahead of the first write
+#pragma unroll
+        for (int it = 0; it < PER; ++it) {
+            const int i = lane + it * kWave;
             const int r = i / (NP / 4);
             const int c = (i % (NP / 4)) * 4;
-            float* dst = tile + r * LD + c;
-            dst[0] = q.x;
-            dst[1] = q.y;
-            dst[2] = q.z;
-            dst[3] = q.w;
+            if (rows == kWave || i < total4) {
+                float* dst = tile + r * LD + c;
+                dst[0] = q[it].x; dst[1] = q[it].y; dst[2] = q[it].z; dst[3] = q[it].w;
+            }
         }
     } else {
         const int total = rows * N;
