@@ -1,10 +1,12 @@
 // Router logits l = x W_r^T (Section 2: a learned router produces logits l(x) in R^N),
 // fp32 accumulation and fp32 output.
 //
-// bf16: one block of 4 waves per 16 tokens; wave w owns experts [16w, 16w + 16) and runs
-// v_mfma_f32_16x16x32_bf16 over the full d, reading its fragments straight from global
-// memory (the 16 x d slice of x is shared by the 4 waves through L1/L2; W_r (N x d) stays in
-// L2 across blocks).  N <= 64.
+// bf16: one block of 4 waves per 16 tokens.  The 32-deep k-steps are dealt round-robin to
+// the waves, so each wave reads a distinct quarter of the 16 x d slice of x (x is read once)
+// and the matching columns of all N rows of W_r (which stays in L2 across blocks); each wave
+// runs 4 v_mfma_f32_16x16x32_bf16 chains (16 experts each) with its loads four steps ahead
+// of their use, and the 4 partial 16 x N tiles are summed in LDS in a fixed order.
+// N <= 64, d % 32 == 0.
 // fp32: one thread per (token, expert) dot product (the small fp32 configuration).
 #include "common.h"
 
@@ -12,46 +14,85 @@ namespace elb {
 
 namespace {
 
-__global__ __launch_bounds__(256) void router_bf16(const bf16_t* __restrict__ x,
-                                                   const bf16_t* __restrict__ Wr, int64_t T,
-                                                   int d, int N, float* __restrict__ logits) {
+constexpr int RW = 4;  // waves per router block
+
+__global__ __launch_bounds__(64 * RW) void router_bf16(const bf16_t* __restrict__ x,
+                                                      const bf16_t* __restrict__ Wr, int64_t T,
+                                                      int d, int N, float* __restrict__ logits) {
+    __shared__ float part[RW][16][65];  // per-wave partial logits (padded rows)
     const int lane = threadIdx.x & 63;
     const int w = threadIdx.x >> 6;
     const int64_t t0 = (int64_t)blockIdx.x * 16;
-    const int n0 = w * 16;
-    if (n0 >= N) return;  // no barriers in this kernel
     const int l16 = lane & 15;
     const int kq = (lane >> 4) * 8;
     const int64_t ta = t0 + l16;
     const bool arow = ta < T;
-    const bool brow = n0 + l16 < N;
     const bf16_t* ap = x + (arow ? ta : 0) * d + kq;
-    const bf16_t* bp = Wr + (int64_t)(brow ? n0 + l16 : 0) * d + kq;
-    const bf16x8_t zero = {};
-    f32x4_t acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = {0.f, 0.f, 0.f, 0.f};
-    int k0 = 0;
-    for (; k0 + 64 <= d; k0 += 64) {
-        bf16x8_t a0 = *reinterpret_cast<const bf16x8_t*>(ap + k0);
-        bf16x8_t b0 = *reinterpret_cast<const bf16x8_t*>(bp + k0);
-        bf16x8_t a1 = *reinterpret_cast<const bf16x8_t*>(ap + k0 + 32);
-        bf16x8_t b1 = *reinterpret_cast<const bf16x8_t*>(bp + k0 + 32);
-        if (!arow) { a0 = zero; a1 = zero; }
-        if (!brow) { b0 = zero; b1 = zero; }
-        acc0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a0, b0, acc0, 0, 0, 0);
-        acc1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a1, b1, acc1, 0, 0, 0);
+    const bf16_t* bp[4];
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+        const int n = 16 * g + l16;
+        bp[g] = Wr + (int64_t)(n < N ? n : 0) * d + kq;
     }
-    for (; k0 < d; k0 += 32) {
-        bf16x8_t a0 = *reinterpret_cast<const bf16x8_t*>(ap + k0);
-        bf16x8_t b0 = *reinterpret_cast<const bf16x8_t*>(bp + k0);
-        if (!arow) a0 = zero;
-        if (!brow) b0 = zero;
-        acc0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a0, b0, acc0, 0, 0, 0);
+    f32x4_t acc[4];
+#pragma unroll
+    for (int g = 0; g < 4; ++g) acc[g] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    // wave w takes the 32-deep k-steps w, w + RW, w + 2 RW, ... (its steps j = 0, 1, ...).  A
+    // ring of R register slots keeps R - 1 steps in flight: step j lives in slot j % R, and
+    // while step j is multiplied, step j + R - 1 is loaded into the slot step j - 1 has just
+    // freed.  Unrolled by R, so every slot index is a constant.
+    constexpr int R = 5;
+    const int nsteps = d / 32;
+    const int mine = (nsteps - w + RW - 1) / RW;  // steps of this wave
+    bf16x8_t ra[R], rb[R][4];
+    auto load = [&](int slot_j, bf16x8_t& a, bf16x8_t (&bb)[4]) {
+        const int k0 = (slot_j < mine ? w + RW * slot_j : 0) * 32;  // past the end: step 0
+        a = *reinterpret_cast<const bf16x8_t*>(ap + k0);
+#pragma unroll
+        for (int g = 0; g < 4; ++g) bb[g] = *reinterpret_cast<const bf16x8_t*>(bp[g] + k0);
+    };
+    // rows past T and experts past N read row 0 and give logits that are never written
+    auto mma = [&](const bf16x8_t& a, const bf16x8_t (&bb)[4]) {
+#pragma unroll
+        for (int g = 0; g < 4; ++g)
+            acc[g] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, bb[g], acc[g], 0, 0, 0);
+    };
+#pragma unroll
+    for (int p = 0; p < R - 1; ++p) load(p, ra[p], rb[p]);
+    int i = 0;
+    for (; i + R <= mine; i += R) {
+#pragma unroll
+        for (int p = 0; p < R; ++p) {
+            const int q = (p + R - 1) % R;
+            load(i + p + R - 1, ra[q], rb[q]);
+            mma(ra[p], rb[p]);
+        }
     }
+#pragma unroll
+    for (int p = 0; p < R; ++p) {  // the last steps (fewer than R)
+        if (i + p < mine) {
+            const int q = (p + R - 1) % R;
+            load(i + p + R - 1, ra[q], rb[q]);
+            mma(ra[p], rb[p]);
+        }
+    }
+
+    // sum the waves' partial tiles in a fixed order (deterministic)
     const int rq = (lane >> 4) * 4;
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-        const int64_t t = t0 + rq + r;
-        if (t < T && brow) logits[t * N + n0 + l16] = acc0[r] + acc1[r];
+    for (int g = 0; g < 4; ++g)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) part[w][rq + r][16 * g + l16] = acc[g][r];
+    __syncthreads();
+#pragma unroll
+    for (int q = 0; q < 1024 / (64 * RW); ++q) {
+        const int o = threadIdx.x + 64 * RW * q;  // output (token o / 64, expert o % 64)
+        const int tr = o >> 6, n = o & 63;
+        const int64_t t = t0 + tr;
+        float v = part[0][tr][n];
+#pragma unroll
+        for (int ww = 1; ww < RW; ++ww) v += part[ww][tr][n];
+        if (t < T && n < N) logits[t * N + n] = v;
     }
 }
 
@@ -76,7 +117,7 @@ hipError_t launch_router(const void* x, const void* Wr, int64_t T, int d, int N,
     if (T == 0) return hipSuccess;
     if (dtype == ELB_BF16) {
         ProfileScope prof("router_bf16", s);
-        hipLaunchKernelGGL(router_bf16, dim3((unsigned)((T + 15) / 16)), dim3(256), 0, s,
+        hipLaunchKernelGGL(router_bf16, dim3((unsigned)((T + 15) / 16)), dim3(64 * RW), 0, s,
                            (const bf16_t*)x, (const bf16_t*)Wr, T, d, N, logits);
     } else {
         ProfileScope prof("router_f32", s);

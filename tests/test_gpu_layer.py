@@ -67,8 +67,11 @@ def test_router_logits_f32_tiny():
     assert rel_err_rows(lg, O.router_logits(L.x, L.W_router)).max() < 1e-5
 
 
-def test_router_ragged_tokens_and_experts():
-    L = synth.moe_layer(37, 96, 50, 64, dtype="bf16", seed=3)
+@pytest.mark.parametrize("T,d,N", [(37, 96, 50), (33, 32, 64), (300, 320, 64), (5, 544, 3)])
+def test_router_ragged_tokens_and_experts(T, d, N):
+    """Ragged token counts (not a multiple of 16), expert counts, and d with no whole 64-deep
+    k-step (32), a trailing half step (96, 544) or fewer steps than the load ring (320)."""
+    L = synth.moe_layer(T, d, N, 64, dtype="bf16", seed=T + d)
     lg = cpu(B.elb_router_logits(to_gpu(L.x, BF), to_gpu(L.W_router, BF)))
     assert rel_err_rows(lg, O.router_logits(L.x, L.W_router)).max() < 1e-5
 
