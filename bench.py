@@ -93,9 +93,34 @@ def routing_only(B, torch, T=65536, N=64, K=8, nbuf=32, iters=64):
     us = ms / cnt * 1e3
     nbytes = T * N * 4 + T * (4 + 4 * K + 4 * K)
     gbs = nbytes / (us * 1e-6) / 1e9
-    return {"workload": "routing-only T=%d N=%d K=%d planted logits" % (T, N, K),
-            "kernel": "route", "us": round(us, 3), "bytes": nbytes, "GB/s": round(gbs, 1),
-            "peak": PEAK_HBM_GBS, "frac": round(gbs / PEAK_HBM_GBS, 4)}
+    out = {"workload": "routing-only T=%d N=%d K=%d planted logits" % (T, N, K),
+           "kernel": "route", "us": round(us, 3), "bytes": nbytes, "GB/s": round(gbs, 1),
+           "peak": PEAK_HBM_GBS, "frac": round(gbs / PEAK_HBM_GBS, 4)}
+    # variable-k dispatch of that routing (histogram, scan, scatter)
+    for _ in range(4):
+        B.elb_dispatch(k, ids, N)
+    torch.cuda.synchronize()
+    B.elb_profile_read()
+    B.elb_profile_enable(True)
+    for _ in range(iters):
+        counts = B.elb_dispatch(k, ids, N)[0]
+    torch.cuda.synchronize()
+    B.elb_profile_enable(False)
+    dk = {n: v[0] / v[1] * 1e3 for n, v in B.elb_profile_read().items()}
+    dus = sum(dk.values())
+    sum_k = int(k.sum().item())
+    dbytes = dispatch_bytes(T, N, K, sum_k)
+    out["dispatch"] = {"kernels_us": {n: round(v, 2) for n, v in dk.items()}, "us": round(dus, 2),
+                       "bytes": dbytes, "GB/s": round(dbytes / (dus * 1e-6) / 1e9, 1),
+                       "frac": round(dbytes / (dus * 1e-6) / 1e9 / PEAK_HBM_GBS, 4),
+                       "sum_k": sum_k}
+    return out
+
+
+def dispatch_bytes(T, N, K, sum_k):
+    """Algorithmic bytes of the dispatch: reads k [T] and ids [T, K]; writes counts [N],
+    offsets [N + 1], row_token [sum k] and inv [T, K] (int32)."""
+    return 4 * (T + T * K) + 4 * (N + N + 1 + sum_k + T * K)
 
 
 GATE_UP_KERNEL = "gemm_bf16_dma<0>"    # device function behind "gemm_gate_up_bf16"
@@ -277,6 +302,30 @@ def main():
             (ms - ms_top) / ms_top * 100, 2),
         "paper_context": "the paper reports a 5.3% average latency reduction on OLMoE on one "
                          "NVIDIA H200 (context only)",
+    }
+    def row(kind, us, work, unit_peak):
+        if us is None or us <= 0:
+            return None
+        rate = work / (us * 1e-6)
+        if kind == "hbm":
+            return {"bound": "hbm", "us": round(us, 2), "bytes": int(work),
+                    "GB/s": round(rate / 1e9, 1), "frac": round(rate / 1e9 / unit_peak, 4)}
+        return {"bound": "mfma", "us": round(us, 2), "flop": work,
+                "TFLOP/s": round(rate / 1e12, 1), "frac": round(rate / 1e12 / unit_peak, 4)}
+    us_of = lambda name: (kern.get(name) or 0) * 1e3
+    res["rows"] = {
+        "router (x W_r^T, fp32 logits)": row(
+            "hbm", us_of("router_bf16"), 2 * T * d + 2 * N * d + 4 * T * N, PEAK_HBM_GBS),
+        "routing (softmax, sort, elbow, cap, weights)": row(
+            "hbm", us_of("route"), 4 * T * N + T * (4 + 8 * K), PEAK_HBM_GBS),
+        "dispatch (histogram, scan, scatter)": row(
+            "hbm", us_of("dispatch_count") + us_of("dispatch_scan") + us_of("dispatch_scatter"),
+            dispatch_bytes(T, N, K, sum_k), PEAK_HBM_GBS),
+        "gate/up GEMM + SwiGLU": row("mfma", us_g1, flop_g1, PEAK_BF16_TFLOPS),
+        "down GEMM": row("mfma", us_of("gemm_down_bf16"), 2.0 * d * m * sum_k,
+                         PEAK_BF16_TFLOPS),
+        "combine (weighted, rank order)": row(
+            "hbm", us_of("combine_bf16"), 2 * sum_k * d + 2 * T * d + 8 * T * K, PEAK_HBM_GBS),
     }
     from paper_2608_04401_amd import stats
     res["load_balance"] = {k2: (round(v, 5) if isinstance(v, float) else v) for k2, v in
