@@ -3,13 +3,14 @@
 // Three launches, deterministic, no atomics:
 //   count   one lane per token; a wave ORs each token's selected experts into a 64-bit mask
 //           and, per expert, counts the wave's tokens with one ballot + popcount.  The
-//           per-wave counts form a [groups, N] histogram.
-//   scan    one block: for every expert, an exclusive prefix over groups (the base of each
-//           group inside the expert's list), the expert totals, their exclusive prefix
-//           (list offsets) and the grouped GEMM's M-tile offsets.
-//   scatter one lane per token again: the rank of a token inside its group's share of
-//           expert e is the popcount of the expert's ballot below the lane; the row is
-//           offsets[e] + base[group, e] + rank.  Rows within an expert are therefore in
+//           per-wave counts form an expert-major [N, groups] histogram.
+//   scan    one block per expert: an exclusive prefix over groups (the base of each group
+//           inside the expert's list) and the expert's total.
+//   scatter one lane per token again.  Each wave first forms the exclusive prefix of the
+//           expert totals (list offsets) and of their M-tile counts with a wave scan (block
+//           0 also writes them out); the rank of a token inside its group's share of expert
+//           e is the popcount of the expert's ballot below the lane, and its row is
+//           offsets[e] + base[e, group] + rank.  Rows within an expert are therefore in
 //           increasing token order.
 // Requires N <= 64 (one mask bit per expert).
 #include "common.h"
@@ -47,75 +48,54 @@ __global__ __launch_bounds__(256) void dispatch_count(const int* __restrict__ k,
         const int c = __popcll(b);
         if (lane == e) mine = c;
     }
-    if (lane < N) hist[g * N + lane] = mine;
+    if (lane < N) hist[(int64_t)lane * groups + g] = mine;
 }
 
-// one block of 1024 threads: thread (e = tid % 64, part = tid / 64)
+// one block per expert e: exclusive prefix of hist[e, :] over the groups, in place
 __global__ __launch_bounds__(1024) void dispatch_scan(int* __restrict__ hist, int64_t groups,
-                                                     int N, int* __restrict__ counts,
-                                                     int* __restrict__ offsets,
-                                                     int* __restrict__ tile_off,
-                                                     int tile_rows) {
-    constexpr int kParts = 16;
-    __shared__ int part_sum[kParts][64];
-    __shared__ int part_base[kParts][64];
-    __shared__ int tot[64];
-    const int e = threadIdx.x & 63;
-    const int part = threadIdx.x >> 6;
-    const int64_t per = (groups + kParts - 1) / kParts;
-    const int64_t g0 = part * per;
-    const int64_t g1 = (g0 + per < groups) ? g0 + per : groups;
+                                                     int* __restrict__ counts) {
+    __shared__ int wsum[16];
+    const int e = blockIdx.x;
+    const int tid = threadIdx.x;
+    const int lane = tid & (kWave - 1);
+    const int wv = tid >> 6;
+    int* h = hist + (int64_t)e * groups;
+    const int64_t chunk = (groups + 1023) / 1024;  // consecutive groups per thread
+    const int64_t g0 = tid * chunk;
+    const int64_t g1 = (g0 + chunk < groups) ? g0 + chunk : groups;
     int s = 0;
-    if (e < N)
-        for (int64_t g = g0; g < g1; ++g) s += hist[g * N + e];
-    part_sum[part][e] = s;
+    for (int64_t g = g0; g < g1; ++g) s += h[g];
+    // block-wide exclusive scan of s: within the wave, then over the 16 wave totals
+    int incl = s;
+    for (int dd = 1; dd < kWave; dd <<= 1) {
+        const int o = __shfl_up(incl, dd);
+        if (lane >= dd) incl += o;
+    }
+    if (lane == kWave - 1) wsum[wv] = incl;
     __syncthreads();
-    if (part == 0) {
-        int run = 0;
-        for (int p = 0; p < kParts; ++p) {
-            part_base[p][e] = run;
-            run += part_sum[p][e];
-        }
-        tot[e] = (e < N) ? run : 0;
+    int wbase = 0, total = 0;
+    for (int q = 0; q < 16; ++q) {
+        const int v = wsum[q];
+        wbase += (q < wv) ? v : 0;
+        total += v;
     }
-    __syncthreads();
-    if (e < N) {
-        int run = part_base[part][e];
-        for (int64_t g = g0; g < g1; ++g) {
-            const int c = hist[g * N + e];
-            hist[g * N + e] = run;  // exclusive base of group g inside expert e's list
-            run += c;
-        }
+    int run = wbase + incl - s;
+    for (int64_t g = g0; g < g1; ++g) {
+        const int c = h[g];
+        h[g] = run;  // exclusive base of group g inside expert e's list
+        run += c;
     }
-    if (threadIdx.x < 64) {  // wave 0: offsets and tile offsets over experts
-        const int c = tot[e];
-        const int tiles = (c + tile_rows - 1) / tile_rows;
-        int incl = c, tincl = tiles;
-        for (int d = 1; d < 64; d <<= 1) {
-            const int o = __shfl_up(incl, d);
-            const int to = __shfl_up(tincl, d);
-            if (e >= d) {
-                incl += o;
-                tincl += to;
-            }
-        }
-        if (e < N) {
-            counts[e] = c;
-            offsets[e] = incl - c;
-            tile_off[e] = tincl - tiles;
-        }
-        if (e == N - 1) {
-            offsets[N] = incl;
-            tile_off[N] = tincl;
-        }
-    }
+    if (tid == 0) counts[e] = total;
 }
 
 __global__ __launch_bounds__(256) void dispatch_scatter(const int* __restrict__ k,
                                                         const int* __restrict__ ids, int64_t T,
                                                         int N, int K,
                                                         const int* __restrict__ hist,
-                                                        const int* __restrict__ offsets,
+                                                        const int* __restrict__ counts,
+                                                        int* __restrict__ offsets,
+                                                        int* __restrict__ tile_off,
+                                                        int tile_rows,
                                                         int* __restrict__ row_token,
                                                         int* __restrict__ inv) {
     __shared__ int pos[4][kWave][kWave + 1];
@@ -124,11 +104,34 @@ __global__ __launch_bounds__(256) void dispatch_scatter(const int* __restrict__ 
     const int64_t g = (int64_t)blockIdx.x * 4 + wv;
     const int64_t t = g * kWave + lane;
     const int64_t groups = (T + kWave - 1) / kWave;
+    // expert list offsets and M-tile offsets: exclusive prefixes over the experts (lane e)
+    const int c = (lane < N) ? counts[lane] : 0;
+    const int tiles = (c + tile_rows - 1) / tile_rows;
+    int incl = c, tincl = tiles;
+    for (int dd = 1; dd < kWave; dd <<= 1) {
+        const int o = __shfl_up(incl, dd);
+        const int to = __shfl_up(tincl, dd);
+        if (lane >= dd) {
+            incl += o;
+            tincl += to;
+        }
+    }
+    const int off_mine = incl - c;
+    if (blockIdx.x == 0 && wv == 0) {
+        if (lane < N) {
+            offsets[lane] = off_mine;
+            tile_off[lane] = tincl - tiles;
+        }
+        if (lane == N - 1) {
+            offsets[N] = incl;
+            tile_off[N] = tincl;
+        }
+    }
     if (g >= groups) return;  // wave-uniform; no block barrier in this kernel
     const bool valid = t < T;
     const uint64_t mask = token_mask(k, ids, t, N, K, valid);
     // lane e holds the first row of expert e that belongs to this group
-    const int base_mine = (lane < N) ? offsets[lane] + hist[g * N + lane] : 0;
+    const int base_mine = (lane < N) ? off_mine + hist[(int64_t)lane * groups + g] : 0;
     const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
     for (int e = 0; e < N; ++e) {
         const bool has = (mask >> e) & 1ull;
@@ -156,7 +159,8 @@ hipError_t launch_dispatch(const int* k, const int* ids, int64_t T, int N, int K
                            int* offsets, int* row_token, int* inv, int* hist, int* tile_off,
                            int tile_rows, hipStream_t s) {
     const int64_t groups = dispatch_groups(T);
-    const unsigned blocks = (unsigned)((groups + 3) / 4);
+    // at least one scatter block, which also writes offsets and tile_off (also when T == 0)
+    const unsigned blocks = (unsigned)((groups + 3) / 4 > 0 ? (groups + 3) / 4 : 1);
     {
         ProfileScope prof("dispatch_count", s);
         if (T > 0)
@@ -165,14 +169,13 @@ hipError_t launch_dispatch(const int* k, const int* ids, int64_t T, int N, int K
     }
     {
         ProfileScope prof("dispatch_scan", s);
-        hipLaunchKernelGGL(dispatch_scan, dim3(1), dim3(1024), 0, s, hist, groups, N, counts,
-                           offsets, tile_off, tile_rows);
+        hipLaunchKernelGGL(dispatch_scan, dim3((unsigned)N), dim3(1024), 0, s, hist, groups,
+                           counts);
     }
     {
         ProfileScope prof("dispatch_scatter", s);
-        if (T > 0)
-            hipLaunchKernelGGL(dispatch_scatter, dim3(blocks), dim3(256), 0, s, k, ids, T, N, K,
-                               hist, offsets, row_token, inv);
+        hipLaunchKernelGGL(dispatch_scatter, dim3(blocks), dim3(256), 0, s, k, ids, T, N, K,
+                           hist, counts, offsets, tile_off, tile_rows, row_token, inv);
     }
     return hipGetLastError();
 }
