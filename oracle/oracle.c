@@ -33,6 +33,10 @@
  *     renormalised over the selected set (renorm = 1 renormalises instead).
  *   - fixed top-K routing (the paper's baseline) is the same path with k = K.
  *
+ *   - elbow angle (Section 2.3): taken as 180 degrees when the elbow is the first point.
+ *   - tail randomisation (Section 2.2): the random tail is drawn from the experts outside
+ *     the elbow's selection with one caller-supplied uniform value per (token, expert).
+ *
  * Parity pins for every function here live in tests/test_oracle_*.py (hand-worked
  * curves, exact-rational brute force, invariants, the load-balance theorem, and special
  * cases that reduce to library routines).
@@ -45,7 +49,7 @@
 #define ORC_MODE_ELBOW 0
 #define ORC_MODE_TOPK 1
 
-int orc_version(void) { return 1; }
+int orc_version(void) { return 2; }
 
 /* Order indices by (key descending, index ascending): a plain insertion sort. */
 static void order_desc(const double *key, int N, int *sigma)
@@ -176,6 +180,140 @@ int orc_route_from_probs(const double *p, long T, int N, int K, double eps, int 
                        competitor ? &competitor[t] : NULL);
     }
     return 0;
+}
+
+/*
+ * Elbow angle (Section 2.3): the angle at the elbow point (x'_e, p'_e) of the normalised
+ * curve between the first normalised point (0,0) and the last (1,1):
+ *   theta = arccos( v1 . v2 / (|v1| |v2|) ),  v1 = (-x'_e, -p'_e),  v2 = (1 - x'_e, 1 - p'_e),
+ * with e the uncapped elbow index (the argmax of D over all i, first index on ties) and
+ * p'_e the flipped normalisation of the routing step.  In degrees.  When e = 0 the elbow
+ * point is the first point itself and v1 = 0: the angle is taken as 180 degrees (a curve
+ * with no point below the chord has no elbow).
+ */
+static void elbow_angle_one(const double *p, const int *sigma, int N, double eps, int *e_out,
+                            double *theta)
+{
+    double hi = p[sigma[0]];
+    double lo = p[sigma[N - 1]];
+    double R = hi - lo + eps;
+    int e = 0;
+    double best = 0.0; /* D_0 = 0 */
+    for (int i = 1; i < N; ++i) {
+        double yi = (hi - p[sigma[i]]) / R;         /* normalised probability */
+        double xi = (double)i / (double)(N - 1);   /* normalised index */
+        if (yi - xi > best) { best = yi - xi; e = i; }
+    }
+    double xe = (double)e / (double)(N - 1);
+    double ye = (hi - p[sigma[e]]) / R;
+    double v1x = -xe, v1y = -ye, v2x = 1.0 - xe, v2y = 1.0 - ye;
+    double n1 = sqrt(v1x * v1x + v1y * v1y), n2 = sqrt(v2x * v2x + v2y * v2y);
+    double th;
+    if (e == 0 || n1 == 0.0 || n2 == 0.0) {
+        th = 180.0;
+    } else {
+        double c = (v1x * v2x + v1y * v2y) / (n1 * n2);
+        if (c > 1.0) c = 1.0;
+        if (c < -1.0) c = -1.0;
+        th = acos(c) * (180.0 / acos(-1.0));
+    }
+    *e_out = e;
+    *theta = th;
+}
+
+/* softmax of one row of fp32 logits into p (fp64); returns 0 if no logit is finite */
+static int softmax_row(const float *lrow, int N, double *l, double *p)
+{
+    for (int j = 0; j < N; ++j) l[j] = (double)lrow[j];
+    double mx = -INFINITY;
+    for (int j = 0; j < N; ++j) if (l[j] > mx) mx = l[j];
+    if (!isfinite(mx)) return 0;
+    double s = 0.0;
+    for (int j = 0; j < N; ++j) { p[j] = exp(l[j] - mx); s += p[j]; }
+    for (int j = 0; j < N; ++j) p[j] /= s;
+    return 1;
+}
+
+/* Elbow index e[T] (uncapped) and angle theta[T] (degrees) from fp32 logits [T, N]. */
+int orc_elbow_angle(const float *logits, long T, int N, double eps, int *e, double *theta)
+{
+    if (T < 0 || N < 2 || !(eps >= 0.0)) return 1;
+    int bad = 0;
+#pragma omp parallel for schedule(static) reduction(| : bad)
+    for (long t = 0; t < T; ++t) {
+        double l[N], p[N];
+        int sigma[N];
+        if (!softmax_row(logits + t * N, N, l, p)) { bad = 1; continue; }
+        order_desc(l, N, sigma);
+        elbow_angle_one(p, sigma, N, eps, &e[t], &theta[t]);
+    }
+    return bad ? 2 : 0;
+}
+
+/* The same on given probability vectors p[T, N] (sort key p, ties by lower id). */
+int orc_elbow_angle_from_probs(const double *p, long T, int N, double eps, int *e,
+                               double *theta)
+{
+    if (T < 0 || N < 2 || !(eps >= 0.0)) return 1;
+    for (long t = 0; t < T; ++t) {
+        int sigma[N];
+        order_desc(p + t * N, N, sigma);
+        elbow_angle_one(p + t * N, sigma, N, eps, &e[t], &theta[t]);
+    }
+    return 0;
+}
+
+/*
+ * Tail randomisation (Section 2.2, the signal/noise check): the elbow's k = min(e + 1, K)
+ * experts keep ranks 0..k-1; the other K - k slots are filled with experts drawn uniformly
+ * from those outside the elbow's selection (equivalently, from the ranks >= k).  The draw is
+ * an input: rand[T, N] holds one value per (token, expert); the drawn experts are the K - k
+ * non-selected ones with the smallest rand (ties: lower id), in increasing order of rand.
+ * Weights are the experts' own probabilities p (renorm = 1: over the K experts).
+ * Outputs k_elbow[T] (where the random tail starts), ids[T, K], w[T, K]: all K slots are
+ * filled.
+ */
+int orc_route_tail_random(const float *logits, const float *rand, long T, int N, int K,
+                          double eps, int renorm, int *k_elbow, int *ids, double *w)
+{
+    if (check_params(T, N, K, eps, ORC_MODE_ELBOW)) return 1;
+    int bad = 0;
+#pragma omp parallel for schedule(static) reduction(| : bad)
+    for (long t = 0; t < T; ++t) {
+        double l[N], p[N];
+        int sigma[N], kk;
+        double wtmp[K];
+        int itmp[K];
+        if (!softmax_row(logits + t * N, N, l, p)) { bad = 1; continue; }
+        order_desc(l, N, sigma);
+        select_experts(p, sigma, N, K, eps, ORC_MODE_ELBOW, 0, &kk, itmp, wtmp, NULL, NULL,
+                       NULL);
+        int used[N];
+        for (int c = 0; c < N; ++c) used[c] = 0;
+        for (int j = 0; j < kk; ++j) used[sigma[j]] = 1;
+        for (int j = 0; j < K; ++j) {
+            int c;
+            if (j < kk) {
+                c = sigma[j];
+            } else {
+                c = -1;
+                for (int q = 0; q < N; ++q) {
+                    if (used[q]) continue;
+                    if (c < 0 || rand[t * N + q] < rand[t * N + c]) c = q;
+                }
+                used[c] = 1;
+            }
+            ids[t * K + j] = c;
+            w[t * K + j] = p[c];
+        }
+        if (renorm) {
+            double s = 0.0;
+            for (int j = 0; j < K; ++j) s += w[t * K + j];
+            for (int j = 0; j < K; ++j) w[t * K + j] /= s;
+        }
+        k_elbow[t] = kk;
+    }
+    return bad ? 2 : 0;
 }
 
 /* Router logits of one token, l = W_r x (the router is a bias-free linear layer). */

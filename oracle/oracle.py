@@ -77,6 +77,10 @@ class OracleLib:
                                         C.c_int, C.c_double, C.c_int, C.c_int, P, C.c_long,
                                         P, P, P, P, P, P]
         lib.orc_dispatch.argtypes = [P, P, C.c_long, C.c_int, C.c_int, P, P, P, P]
+        lib.orc_elbow_angle.argtypes = [P, C.c_long, C.c_int, C.c_double, P, P]
+        lib.orc_elbow_angle_from_probs.argtypes = lib.orc_elbow_angle.argtypes
+        lib.orc_route_tail_random.argtypes = [P, P, C.c_long, C.c_int, C.c_int, C.c_double,
+                                              C.c_int, P, P, P]
         self.lib = lib
         self.path = path
 
@@ -124,6 +128,46 @@ class OracleLib:
             pp = pp[None, :]
         return self._route(self.lib.orc_route_from_probs, pp, pp.shape[1], K, eps, mode,
                            renorm)
+
+    def elbow_angle(self, logits, eps: float = DEFAULT_EPS):
+        """Uncapped elbow index e [T] (int32) and elbow angle theta [T] (degrees, float64)
+        of fp32 logits [T, N] (Section 2.3)."""
+        lg = _f32(logits)
+        return self._angle(self.lib.orc_elbow_angle, lg, eps)
+
+    def elbow_angle_from_probs(self, p, eps: float = DEFAULT_EPS):
+        """The same on given probability vectors [T, N] (float64)."""
+        pp = np.ascontiguousarray(p, dtype=np.float64)
+        if pp.ndim == 1:
+            pp = pp[None, :]
+        return self._angle(self.lib.orc_elbow_angle_from_probs, pp, eps)
+
+    def _angle(self, fn, arr, eps):
+        T, N = arr.shape
+        e = np.empty(T, np.int32)
+        th = np.empty(T, np.float64)
+        rc = fn(_ptr(arr), T, N, eps, _ptr(e), _ptr(th))
+        if rc != 0:
+            raise ValueError("oracle elbow angle failed with code %d" % rc)
+        return e, th
+
+    def route_tail_random(self, logits, rand, K: int, eps: float = DEFAULT_EPS,
+                          renorm: bool = False):
+        """Tail randomisation: the elbow's k experts, then K - k experts outside them drawn
+        by the smallest rand [T, N] values.  -> (k_elbow [T], ids [T, K], w [T, K])."""
+        lg = _f32(logits)
+        rd = _f32(rand)
+        T, N = lg.shape
+        if rd.shape != lg.shape:
+            raise ValueError("rand must have the logits' shape")
+        k = np.empty(T, np.int32)
+        ids = np.empty((T, K), np.int32)
+        w = np.empty((T, K), np.float64)
+        rc = self.lib.orc_route_tail_random(_ptr(lg), _ptr(rd), T, N, K, eps, int(renorm),
+                                            _ptr(k), _ptr(ids), _ptr(w))
+        if rc != 0:
+            raise ValueError("oracle tail randomisation failed with code %d" % rc)
+        return k, ids, w
 
     def router_logits(self, x, W_router) -> np.ndarray:
         """fp64 logits [T, N] = x W_r^T."""
@@ -213,3 +257,15 @@ def dispatch(*a, **kw):
 
 def moe_forward(*a, **kw) -> LayerResult:
     return _lib().moe_forward(*a, **kw)
+
+
+def elbow_angle(*a, **kw):
+    return _lib().elbow_angle(*a, **kw)
+
+
+def elbow_angle_from_probs(*a, **kw):
+    return _lib().elbow_angle_from_probs(*a, **kw)
+
+
+def route_tail_random(*a, **kw):
+    return _lib().route_tail_random(*a, **kw)

@@ -38,6 +38,16 @@ MUTATIONS = {
     "weight_dropped": ("acc[c] += w[r * K + j] * o[c];", "acc[c] += o[c];"),
     "residual_dropped": ("acc[c] = residual ? (double)residual[t * d + c] : 0.0;",
                          "acc[c] = 0.0;"),
+    # elbow angle (Section 2.3)
+    "angle_v2_reversed": ("v2x = 1.0 - xe, v2y = 1.0 - ye;", "v2x = xe - 1.0, v2y = ye - 1.0;"),
+    "angle_in_radians": ("th = acos(c) * (180.0 / acos(-1.0));", "th = acos(c);"),
+    "angle_last_index_wins": ("if (yi - xi > best)", "if (yi - xi >= best)"),
+    "angle_point_unflipped": ("double ye = (hi - p[sigma[e]]) / R;",
+                              "double ye = (p[sigma[e]] - lo) / R;"),
+    # tail randomisation (Section 2.2)
+    "tail_largest_draws": ("if (c < 0 || rand[t * N + q] < rand[t * N + c]) c = q;",
+                           "if (c < 0 || rand[t * N + q] > rand[t * N + c]) c = q;"),
+    "tail_may_repeat": ("                if (used[q]) continue;\n", ""),
     "down_transposed": ("const float *wd = Wd + (long)r * m;\n        for (int i = 0; i < m; ++i) acc += (double)wd[i] * h[i];",
                         "for (int i = 0; i < m; ++i) acc += (double)Wd[(long)i * d + r] * h[i];"),
 }
@@ -126,6 +136,41 @@ def run_pins(orc) -> list:
         r = orc.route_from_probs(p, K=8, eps=0.0)
         return r.e[0] == 0 and r.k[0] == 1
 
+    def angle():
+        import math
+        for N, m in ((8, 3), (64, 7)):
+            p = np.full(N, 0.01)
+            p[:m] = (1.0 - 0.01 * (N - m)) / m
+            e, th = orc.elbow_angle_from_probs(p, eps=0.0)
+            if e[0] != m or abs(th[0] - (90 + math.degrees(math.atan(m / (N - 1))))) > 1e-9:
+                return False
+        e, th = orc.elbow_angle_from_probs(np.array([0.5, 0.2, 0.15, 0.1, 0.05]), eps=0.0)
+        if e[0] != 1 or abs(th[0] - math.degrees(math.acos(-59 / math.sqrt(7081)))) > 1e-9:
+            return False
+        lin = np.array([(8 - i) * 2.0 ** -4 for i in range(8)])   # linear: D_i == 0 exactly
+        e, th = orc.elbow_angle_from_probs(lin, eps=0.0)
+        return e[0] == 0 and th[0] == 180.0
+
+    def tail_random():
+        rng = np.random.default_rng(5)
+        T, N, K = 200, 32, 6
+        lg = (-np.cumsum(rng.exponential(1.0, (T, N)), axis=1)).astype(np.float32)  # rank = id
+        k, ids, w = orc.route_tail_random(lg, np.tile(np.arange(N, dtype=np.float32), (T, 1)), K)
+        if not np.array_equal(ids, orc.route(lg, K, mode=O.MODE_TOPK).ids):
+            return False
+        rand = rng.random((T, N), dtype=np.float32)
+        k, ids, w = orc.route_tail_random(lg, rand, K)
+        for t in range(T):
+            tail = ids[t, k[t]:]
+            others = np.setdiff1d(np.arange(N), ids[t])
+            if len(set(ids[t])) != K:
+                return False
+            if len(tail) and rand[t, tail].max() > rand[t, others].min():
+                return False
+        return True
+
+    check("angle", angle)
+    check("tail_random", tail_random)
     check("exact_ties", exact_ties)
     check("golden", golden)
     check("bruteforce", bruteforce)
