@@ -39,9 +39,10 @@ extern "C" {
 
 #define ELB_ABI_VERSION 1
 
-/* Largest supported expert count N and cap K. */
+/* Largest supported expert count N and cap K (any cap up to N: K = N is the uncapped
+   elbow routing). */
 #define ELB_MAX_EXPERTS 64
-#define ELB_MAX_K 16
+#define ELB_MAX_K 64
 
 typedef enum {
     ELB_OK = 0,
@@ -101,6 +102,44 @@ int elb_router_logits(const void *x, const void *W_router, int64_t T, int32_t d,
  */
 int elb_route(const float *logits, int64_t T, int32_t N, const elb_route_params *params,
               int32_t *k, int32_t *ids, float *w, void *stream);
+
+/*
+ * Tail randomisation (Section 2.2): the elbow's k = min(e + 1, K) experts, as elb_route
+ * selects them, followed by K - k further experts drawn uniformly without replacement from
+ * the N - k experts outside that selection, so every token uses exactly K experts.  The draw
+ * is the caller's: `rand[t, c]` is a uniform sample for expert c of token t, and the tail is
+ * the K - k unselected experts with the smallest draws, in increasing draw order (equal
+ * draws: lower expert id first).  With i.i.d. uniform draws this is a uniform draw without
+ * replacement; the caller owns the random stream, so results are reproducible.
+ *   logits  [T, N] float   input
+ *   rand    [T, N] float   input, the draws (any finite values; only their order matters)
+ *   k_elbow [T]    int32   output, the elbow's k (1 <= k <= K)
+ *   ids     [T, K] int32   output, the elbow's experts in descending-probability order,
+ *                          then the tail in increasing draw order; never -1
+ *   w       [T, K] float   output, each expert's own full-softmax probability, or with
+ *                          params->renormalize the probability over the K selected experts
+ * Requirements as elb_route; params->mode = ELB_MODE_TOPK gives k = K and no tail.
+ */
+int elb_route_tail_random(const float *logits, const float *rand, int64_t T, int32_t N,
+                          const elb_route_params *params, int32_t *k_elbow, int32_t *ids,
+                          float *w, void *stream);
+
+/*
+ * Elbow angle (Section 2.3): the angle at the elbow point P_e = (x'_e, p'_e) of the
+ * normalised sorted curve between the vectors to its ends (0,0) and (1,1),
+ *   theta = arccos(v1 . v2 / (|v1| |v2|)),  v1 = -P_e,  v2 = (1,1) - P_e,
+ * in degrees; small angles mark sharp elbows (confident routing), angles near 180 a curve
+ * close to the chord.  e is the uncapped elbow index of elb_route (before min(e + 1, K));
+ * when no point has D_i > 0, e = 0 and theta is taken as 180 (a straight curve).
+ * Every elbow point lies in the unit square, inside the circle whose diameter is the chord
+ * from (0,0) to (1,1), so 90 <= theta <= 180.
+ *   logits [T, N] float   input
+ *   e      [T]    int32   output, 0 <= e <= N - 1 (may be NULL)
+ *   theta  [T]    float   output, degrees (may be NULL)
+ * Requirements: 2 <= N <= ELB_MAX_EXPERTS; eps >= 0 and finite.
+ */
+int elb_elbow_angle(const float *logits, int64_t T, int32_t N, float eps, int32_t *e,
+                    float *theta, void *stream);
 
 /*
  * Variable-k dispatch: expert-major token lists built from a routing (deterministic:

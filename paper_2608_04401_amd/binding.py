@@ -18,7 +18,7 @@ LIB_PATH = os.path.join(_PKG, "libelbow_moe.so")
 
 ELB_F32, ELB_BF16 = 0, 1
 MODE_ELBOW, MODE_TOPK = 0, 1
-MAX_EXPERTS, MAX_K = 64, 16
+MAX_EXPERTS, MAX_K = 64, 64
 
 _lib = None
 
@@ -50,6 +50,9 @@ def lib():
         "elb_last_error": ([], C.c_char_p),
         "elb_router_logits": ([P, P, I64, I32, I32, I32, P, P], C.c_int),
         "elb_route": ([P, I64, I32, C.POINTER(RouteParams), P, P, P, P], C.c_int),
+        "elb_route_tail_random": ([P, P, I64, I32, C.POINTER(RouteParams), P, P, P, P],
+                                  C.c_int),
+        "elb_elbow_angle": ([P, I64, I32, C.c_float, P, P, P], C.c_int),
         "elb_dispatch_workspace_bytes": ([I64, I32], SZ),
         "elb_dispatch": ([P, P, I64, I32, I32, P, P, P, P, P, SZ, P], C.c_int),
         "elb_moe_workspace_bytes": ([I64, I32, I32, I32, I32, I32], SZ),
@@ -145,6 +148,37 @@ def elb_route(logits: torch.Tensor, K: int, eps: float = 1e-8, mode: int = MODE_
     _check("elb_route", lib().elb_route(_ptr(logits), T, N, C.byref(p), _ptr(k), _ptr(ids),
                                         _ptr(w), _stream()))
     return k, ids, w
+
+
+def elb_route_tail_random(logits: torch.Tensor, rand: torch.Tensor, K: int, eps: float = 1e-8,
+                          mode: int = MODE_ELBOW, renormalize: bool = False):
+    """-> (k_elbow [T] int32, ids [T, K] int32, w [T, K] float32); rand [T, N] float32"""
+    _dev(logits, rand)
+    if logits.dtype != torch.float32 or rand.dtype != torch.float32:
+        raise TypeError("logits and rand must be float32")
+    if rand.shape != logits.shape:
+        raise ValueError("rand must have the shape of logits")
+    T, N = logits.shape
+    k = torch.empty(T, dtype=torch.int32, device=logits.device)
+    ids = torch.empty((T, K), dtype=torch.int32, device=logits.device)
+    w = torch.empty((T, K), dtype=torch.float32, device=logits.device)
+    p = RouteParams(K, eps, mode, int(renormalize))
+    _check("elb_route_tail_random", lib().elb_route_tail_random(
+        _ptr(logits), _ptr(rand), T, N, C.byref(p), _ptr(k), _ptr(ids), _ptr(w), _stream()))
+    return k, ids, w
+
+
+def elb_elbow_angle(logits: torch.Tensor, eps: float = 1e-8):
+    """-> (e [T] int32, theta [T] float32 degrees)"""
+    _dev(logits)
+    if logits.dtype != torch.float32:
+        raise TypeError("logits must be float32")
+    T, N = logits.shape
+    e = torch.empty(T, dtype=torch.int32, device=logits.device)
+    theta = torch.empty(T, dtype=torch.float32, device=logits.device)
+    _check("elb_elbow_angle", lib().elb_elbow_angle(_ptr(logits), T, N, eps, _ptr(e),
+                                                    _ptr(theta), _stream()))
+    return e, theta
 
 
 def elb_dispatch(k: torch.Tensor, ids: torch.Tensor, N: int):

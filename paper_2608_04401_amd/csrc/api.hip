@@ -83,8 +83,6 @@ int check_route_params(int N, const elb_route_params* p) {
                     ELB_MAX_EXPERTS);
     if (p->K < 1 || p->K > N)
         return fail(ELB_ERR_INVALID_ARG, "K = %d outside [1, N = %d]", p->K, N);
-    if (p->K > ELB_MAX_K)
-        return fail(ELB_ERR_UNSUPPORTED, "K = %d exceeds ELB_MAX_K = %d", p->K, ELB_MAX_K);
     if (!(p->eps >= 0.f) || !std::isfinite(p->eps))
         return fail(ELB_ERR_INVALID_ARG, "eps = %g must be finite and >= 0", (double)p->eps);
     if (p->mode != ELB_MODE_ELBOW && p->mode != ELB_MODE_TOPK)
@@ -108,8 +106,6 @@ int check_expert_dims(int64_t T, int d, int N, int m, int K, int dtype) {
         return fail(ELB_ERR_UNSUPPORTED, "N = %d exceeds ELB_MAX_EXPERTS = %d", N,
                     ELB_MAX_EXPERTS);
     if (K < 1 || K > N) return fail(ELB_ERR_INVALID_ARG, "K = %d outside [1, N = %d]", K, N);
-    if (K > ELB_MAX_K)
-        return fail(ELB_ERR_UNSUPPORTED, "K = %d exceeds ELB_MAX_K = %d", K, ELB_MAX_K);
     if (d < 1 || m < 1) return fail(ELB_ERR_INVALID_ARG, "d = %d, m = %d must be >= 1", d, m);
     const int g = dtype == ELB_BF16 ? 64 : 16;
     if (d % g || m % g)
@@ -206,6 +202,34 @@ int elb_route(const float* logits, int64_t T, int32_t N, const elb_route_params*
     if (!logits || !k || !ids || !w) return fail(ELB_ERR_INVALID_ARG, "NULL tensor pointer");
     return hip_status(launch_route(logits, T, N, *params, k, ids, w, (hipStream_t)stream),
                       "route");
+}
+
+int elb_route_tail_random(const float* logits, const float* rand, int64_t T, int32_t N,
+                          const elb_route_params* params, int32_t* k_elbow, int32_t* ids,
+                          float* w, void* stream) {
+    g_err.clear();
+    if (T < 0) return fail(ELB_ERR_INVALID_ARG, "T = %lld < 0", (long long)T);
+    if (int rc = check_route_params(N, params)) return rc;
+    if (T == 0) return ELB_OK;
+    if (!logits || !rand || !k_elbow || !ids || !w)
+        return fail(ELB_ERR_INVALID_ARG, "NULL tensor pointer");
+    return hip_status(launch_route_wave(logits, rand, T, N, *params, k_elbow, ids, w, nullptr,
+                                        nullptr, (hipStream_t)stream),
+                      "route_tail_random");
+}
+
+int elb_elbow_angle(const float* logits, int64_t T, int32_t N, float eps, int32_t* e,
+                    float* theta, void* stream) {
+    g_err.clear();
+    if (T < 0) return fail(ELB_ERR_INVALID_ARG, "T = %lld < 0", (long long)T);
+    const elb_route_params p{N, eps, ELB_MODE_ELBOW, 0};
+    if (int rc = check_route_params(N, &p)) return rc;
+    if (T == 0) return ELB_OK;
+    if (!logits) return fail(ELB_ERR_INVALID_ARG, "NULL tensor pointer");
+    if (!e && !theta) return ELB_OK;  // nothing asked for
+    return hip_status(launch_route_wave(logits, nullptr, T, N, p, nullptr, nullptr, nullptr, e,
+                                        theta, (hipStream_t)stream),
+                      "elbow_angle");
 }
 
 size_t elb_dispatch_workspace_bytes(int64_t T, int32_t N) {

@@ -296,7 +296,8 @@ hipError_t launch_route(const float* logits, int64_t T, int N, const elb_route_p
                         int* k, int* ids, float* w, hipStream_t s) {
     if (T == 0) return hipSuccess;
     if (p.K <= 8) return launch_k<8>(logits, T, N, p, k, ids, w, s);
-    return launch_k<ELB_MAX_K>(logits, T, N, p, k, ids, w, s);
+    if (p.K <= kLaneMaxK) return launch_k<kLaneMaxK>(logits, T, N, p, k, ids, w, s);
+    return launch_route_wave(logits, nullptr, T, N, p, k, ids, w, nullptr, nullptr, s);
 }
 
 }  // namespace elb

@@ -145,3 +145,10 @@ def planted_logits(T: int = 65536, N: int = 64, seed=0, m_max: int = 8,
 def gaussian_logits(T: int, N: int, seed=0, std: float = 1.0) -> np.ndarray:
     rng = np.random.default_rng(seed)
     return _normal(rng, (T, N), std)
+
+
+def uniform_draws(T: int, N: int, seed=0) -> np.ndarray:
+    """Uniform [0, 1) float32 draws [T, N], one per (token, expert): the random numbers of
+    tail randomisation, passed in to both sides."""
+    rng = np.random.default_rng([seed, 2 * 10 ** 6])
+    return rng.random((T, N), dtype=np.float32)

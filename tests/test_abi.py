@@ -50,7 +50,7 @@ def _route(T, N, K=8, eps=1e-8, mode=0, renorm=0, ptr=DUMMY, params=True):
     (10, 65, 8, 1e-8, 0, 0, UNSUPPORTED),    # N beyond the kernels
     (10, 64, 0, 1e-8, 0, 0, INVALID),        # K < 1
     (10, 8, 9, 1e-8, 0, 0, INVALID),         # K > N
-    (10, 64, 17, 1e-8, 0, 0, UNSUPPORTED),   # K beyond the kernels
+    (10, 64, 65, 1e-8, 0, 0, INVALID),       # K > N at the largest N
     (10, 64, 8, -1.0, 0, 0, INVALID),        # eps < 0
     (10, 64, 8, float("nan"), 0, 0, INVALID),
     (10, 64, 8, 1e-8, 2, 0, INVALID),        # bad mode
