@@ -25,6 +25,9 @@ sys.path.insert(0, ROOT)
 
 PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0         # MI355X HBM3E
+# a grouped GEMM does 4 d m FLOPs per row on 4 d m bytes of an expert's gate/up weights:
+# compute-bound above this many rows per expert (the bf16 ridge point, FLOP per byte)
+RIDGE_ROWS = PEAK_BF16_TFLOPS * 1e12 / (PEAK_HBM_GBS * 1e9)
 
 WORKLOADS = {
     # name: (T, d, N, m, K)
@@ -258,10 +261,15 @@ def main():
         ms_top, _ = time_layer(B, torch, gpu, K, B.MODE_TOPK, args.steps, args.warmup, False)
         _, kern_top = time_layer(B, torch, gpu, K, B.MODE_TOPK, args.steps, 2, True)
 
-    g1 = "gemm_gate_up_bf16"
+    # the grouped GEMMs' kernels (the small-tile variants carry a "_s" suffix)
+    g1 = next(n for n in kern if n.startswith("gemm_gate_up"))
+    g2 = next(n for n in kern if n.startswith("gemm_down"))
     flop_g1 = 4.0 * d * m * sum_k            # useful FLOPs of the gate/up GEMM per launch
     us_g1 = kern[g1] * 1e3
     achieved = flop_g1 / (us_g1 * 1e-6) / 1e12
+    used = int((counts > 0).sum())           # experts with at least one token
+    # algorithmic HBM bytes of the gate/up GEMM: the used experts' weights, x rows, H out
+    bytes_g1 = used * 2 * m * d * 2 + T * d * 2 + sum_k * m * 2
     traffic = None           # null once the kernel source differs from the one counted
     if args.workload == "olmoe-prefill" and os.path.exists(TRAFFIC_FILE):
         tj = json.load(open(TRAFFIC_FILE))
@@ -285,10 +293,18 @@ def main():
                                "elbow routing capped at K=%d, bf16 weights N(0,0.02), bf16 "
                                "x N(0,1), seed 0" % (args.workload, T, d, N, m, K),
                    "global_batch": T, "K": K},
-        "roofline": {"bound": "mfma", "kernel": g1, "achieved": round(achieved, 1),
-                     "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                     "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": traffic,
-                     "flop_per_launch": flop_g1, "us_per_launch": round(us_g1, 2)},
+        "roofline": ({"bound": "mfma", "kernel": g1, "achieved": round(achieved, 1),
+                      "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                      "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": traffic,
+                      "flop_per_launch": flop_g1, "us_per_launch": round(us_g1, 2)}
+                     if sum_k / N >= RIDGE_ROWS else
+                     {"bound": "hbm", "kernel": g1,
+                      "achieved": round(bytes_g1 / (us_g1 * 1e-6) / 1e9, 1),
+                      "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                      "frac": round(bytes_g1 / (us_g1 * 1e-6) / 1e9 / PEAK_HBM_GBS, 4),
+                      "traffic": traffic, "bytes_per_launch": bytes_g1,
+                      "us_per_launch": round(us_g1, 2)}),
+        "experts_used": used,
         "mean_k": round(sum_k / T, 4),
         "expert_flop_fraction_of_peak": round(flop_all / (sum(
             kern[n] for n in kern if n.startswith("gemm")) * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
@@ -322,8 +338,10 @@ def main():
             "hbm", us_of("dispatch_count") + us_of("dispatch_scan") + us_of("dispatch_scatter"),
             dispatch_bytes(T, N, K, sum_k), PEAK_HBM_GBS),
         "gate/up GEMM + SwiGLU": row("mfma", us_g1, flop_g1, PEAK_BF16_TFLOPS),
-        "down GEMM": row("mfma", us_of("gemm_down_bf16"), 2.0 * d * m * sum_k,
-                         PEAK_BF16_TFLOPS),
+        "gate/up GEMM weight stream": row("hbm", us_g1, bytes_g1, PEAK_HBM_GBS),
+        "down GEMM weight stream": row(
+            "hbm", us_of(g2), used * d * m * 2 + sum_k * (m + d) * 2, PEAK_HBM_GBS),
+        "down GEMM": row("mfma", us_of(g2), 2.0 * d * m * sum_k, PEAK_BF16_TFLOPS),
         "combine (weighted, rank order)": row(
             "hbm", us_of("combine_bf16"), 2 * sum_k * d + 2 * T * d + 8 * T * K, PEAK_HBM_GBS),
     }

@@ -286,12 +286,19 @@ static int experts_impl(const void* x, const void* W_gate_up, const void* W_down
     if (int rc = hip_status(launch_dispatch(k, ids, T, N, K, counts, offsets, row_token, inv,
                                             hist, tile_off, tr, s), "dispatch"))
         return rc;
-    if (int rc = hip_status(launch_gemm_gate_up(x, W_gate_up, row_token, offsets, tile_off, mt,
-                                                tr, d, N, m, dtype, H, s), "gemm_gate_up"))
-        return rc;
-    if (int rc = hip_status(launch_gemm_down(H, W_down, offsets, tile_off, mt, tr, d, N, m,
-                                             dtype, Y, s), "gemm_down"))
-        return rc;
+    if (gemm_use_skinny(dtype, T, K, N, d, m)) {
+        if (int rc = hip_status(launch_gemm_skinny(x, W_gate_up, W_down, row_token, offsets, d,
+                                                   N, m, H, Y, s), "gemm_skinny"))
+            return rc;
+    } else {
+        if (int rc = hip_status(launch_gemm_gate_up(x, W_gate_up, row_token, offsets, tile_off,
+                                                    mt, tr, d, N, m, dtype, H, s),
+                                "gemm_gate_up"))
+            return rc;
+        if (int rc = hip_status(launch_gemm_down(H, W_down, offsets, tile_off, mt, tr, d, N, m,
+                                                 dtype, Y, s), "gemm_down"))
+            return rc;
+    }
     return hip_status(launch_combine(Y, k, inv, w, residual, T, d, K, dtype, y, s), "combine");
 }
 

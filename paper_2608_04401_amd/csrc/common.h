@@ -64,6 +64,12 @@ hipError_t launch_gemm_down(const void* H, const void* Wd, const int* offsets,
                             const int* tile_off, int64_t max_tiles, int tile_rows, int d, int N,
                             int m, int dtype, void* Y, hipStream_t s);
 
+// decode-sized batches: weight-streaming gate/up (+SwiGLU) and down GEMMs, both launched
+bool gemm_use_skinny(int dtype, int64_t T, int K, int N, int d, int m);
+hipError_t launch_gemm_skinny(const void* x, const void* Wgu, const void* Wd,
+                              const int* row_token, const int* offsets, int d, int N, int m,
+                              void* H, void* Y, hipStream_t s);
+
 // combine: y[t] = residual[t] + sum_j w[t, j] Y[inv[t, j]]
 hipError_t launch_combine(const void* Y, const int* k, const int* inv, const float* w,
                           const void* residual, int64_t T, int d, int K, int dtype, void* y,
