@@ -334,6 +334,10 @@ def main():
             "hbm", us_of("router_bf16"), 2 * T * d + 2 * N * d + 4 * T * N, PEAK_HBM_GBS),
         "routing (softmax, sort, elbow, cap, weights)": row(
             "hbm", us_of("route"), 4 * T * N + T * (4 + 8 * K), PEAK_HBM_GBS),
+        # the layer's default for bf16: one kernel, logits kept on chip
+        "router + routing fused": row(
+            "hbm", us_of("router_route_bf16"), 2 * T * d + 2 * N * d + T * (4 + 8 * K),
+            PEAK_HBM_GBS),
         "dispatch (histogram, scan, scatter)": row(
             "hbm", us_of("dispatch_count") + us_of("dispatch_scan") + us_of("dispatch_scatter"),
             dispatch_bytes(T, N, K, sum_k), PEAK_HBM_GBS),
@@ -345,6 +349,7 @@ def main():
         "combine (weighted, rank order)": row(
             "hbm", us_of("combine_bf16"), 2 * sum_k * d + 2 * T * d + 8 * T * K, PEAK_HBM_GBS),
     }
+    res["rows"] = {name: r for name, r in res["rows"].items() if r is not None}
     from paper_2608_04401_amd import stats
     res["load_balance"] = {k2: (round(v, 5) if isinstance(v, float) else v) for k2, v in
                            stats.load_balance_report(counts, counts_top, K, T).items()}

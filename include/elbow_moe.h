@@ -104,6 +104,21 @@ int elb_route(const float *logits, int64_t T, int32_t N, const elb_route_params 
               int32_t *k, int32_t *ids, float *w, void *stream);
 
 /*
+ * Router and routing fused (elb_router_logits followed by elb_route, in one kernel): each
+ * block computes the logits of 16 tokens on the matrix cores, keeps them in LDS and routes
+ * them there with the routing kernel's own per-token code, so k, ids and w are bit-identical
+ * to the two-step path and the logits need not be written to memory.
+ *   x, W_router          as elb_router_logits (ELB_BF16 only, d % 32 == 0)
+ *   params               as elb_route, with K <= 16
+ *   logits_out [T, N]    float output, or NULL to skip writing the logits
+ *   k, ids, w            as elb_route
+ * Other dtypes or caps: ELB_ERR_UNSUPPORTED (use the two calls).
+ */
+int elb_router_route(const void *x, const void *W_router, int64_t T, int32_t d, int32_t N,
+                     int32_t dtype, const elb_route_params *params, float *logits_out,
+                     int32_t *k, int32_t *ids, float *w, void *stream);
+
+/*
  * Tail randomisation (Section 2.2): the elbow's k = min(e + 1, K) experts, as elb_route
  * selects them, followed by K - k further experts drawn uniformly without replacement from
  * the N - k experts outside that selection, so every token uses exactly K experts.  The draw
@@ -180,8 +195,8 @@ int elb_moe_experts(const void *x, const void *W_gate_up, const void *W_down,
                     void *y, void *workspace, size_t workspace_bytes, void *stream);
 
 /*
- * The whole layer: elb_router_logits, elb_route, then elb_moe_experts, on one stream,
- * with no host round trip.  Arguments as above; the optional debug outputs (NULL to
+ * The whole layer: elb_router_logits, elb_route (fused into elb_router_route for bf16 and
+ * K <= 16), then elb_moe_experts, on one stream, with no host round trip.  Arguments as above; the optional debug outputs (NULL to
  * skip) receive the intermediate results of this call:
  *   logits_out [T, N] float, k_out [T], ids_out [T, K], w_out [T, K],
  *   counts_out [N] int32 (assignments per expert).

@@ -50,6 +50,8 @@ def lib():
         "elb_last_error": ([], C.c_char_p),
         "elb_router_logits": ([P, P, I64, I32, I32, I32, P, P], C.c_int),
         "elb_route": ([P, I64, I32, C.POINTER(RouteParams), P, P, P, P], C.c_int),
+        "elb_router_route": ([P, P, I64, I32, I32, I32, C.POINTER(RouteParams), P, P, P, P, P],
+                             C.c_int),
         "elb_route_tail_random": ([P, P, I64, I32, C.POINTER(RouteParams), P, P, P, P],
                                   C.c_int),
         "elb_elbow_angle": ([P, I64, I32, C.c_float, P, P, P], C.c_int),
@@ -148,6 +150,25 @@ def elb_route(logits: torch.Tensor, K: int, eps: float = 1e-8, mode: int = MODE_
     _check("elb_route", lib().elb_route(_ptr(logits), T, N, C.byref(p), _ptr(k), _ptr(ids),
                                         _ptr(w), _stream()))
     return k, ids, w
+
+
+def elb_router_route(x: torch.Tensor, W_router: torch.Tensor, K: int, eps: float = 1e-8,
+                     mode: int = MODE_ELBOW, renormalize: bool = False,
+                     with_logits: bool = False):
+    """-> (k [T], ids [T, K], w [T, K], logits [T, N] or None)"""
+    _dev(x, W_router)
+    T, d = x.shape
+    N = W_router.shape[0]
+    dev = x.device
+    k = torch.empty(T, dtype=torch.int32, device=dev)
+    ids = torch.empty((T, K), dtype=torch.int32, device=dev)
+    w = torch.empty((T, K), dtype=torch.float32, device=dev)
+    logits = torch.empty((T, N), dtype=torch.float32, device=dev) if with_logits else None
+    p = RouteParams(K, eps, mode, int(renormalize))
+    _check("elb_router_route", lib().elb_router_route(
+        _ptr(x), _ptr(W_router), T, d, N, _dtype_code(x), C.byref(p), _ptr(logits), _ptr(k),
+        _ptr(ids), _ptr(w), _stream()))
+    return k, ids, w, logits
 
 
 def elb_route_tail_random(logits: torch.Tensor, rand: torch.Tensor, K: int, eps: float = 1e-8,

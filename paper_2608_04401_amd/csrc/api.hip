@@ -204,6 +204,26 @@ int elb_route(const float* logits, int64_t T, int32_t N, const elb_route_params*
                       "route");
 }
 
+int elb_router_route(const void* x, const void* W_router, int64_t T, int32_t d, int32_t N,
+                     int32_t dtype, const elb_route_params* params, float* logits_out,
+                     int32_t* k, int32_t* ids, float* w, void* stream) {
+    g_err.clear();
+    if (int rc = check_dtype(dtype)) return rc;
+    if (T < 0) return fail(ELB_ERR_INVALID_ARG, "T = %lld < 0", (long long)T);
+    if (int rc = check_route_params(N, params)) return rc;
+    if (d < 1) return fail(ELB_ERR_INVALID_ARG, "d = %d < 1", d);
+    if (!router_route_fusable(dtype, params->K))
+        return fail(ELB_ERR_UNSUPPORTED, "the fused router and routing needs bf16 and K <= %d",
+                    kLaneMaxK);
+    if (d % 32) return fail(ELB_ERR_INVALID_ARG, "bf16 router needs d %% 32 == 0 (d = %d)", d);
+    if (T == 0) return ELB_OK;
+    if (!x || !W_router || !k || !ids || !w)
+        return fail(ELB_ERR_INVALID_ARG, "NULL tensor pointer");
+    return hip_status(launch_router_route(x, W_router, T, d, N, *params, logits_out, k, ids, w,
+                                          (hipStream_t)stream),
+                      "router_route");
+}
+
 int elb_route_tail_random(const float* logits, const float* rand, int64_t T, int32_t N,
                           const elb_route_params* params, int32_t* k_elbow, int32_t* ids,
                           float* w, void* stream) {
@@ -342,10 +362,17 @@ int elb_moe_forward(const void* x, const void* W_router, const void* W_gate_up,
     int* k = k_out ? k_out : (int*)(ws + L.k);
     int* ids = ids_out ? ids_out : (int*)(ws + L.ids);
     float* w = w_out ? w_out : (float*)(ws + L.w);
-    if (int rc = hip_status(launch_router(x, W_router, T, d, N, dtype, logits, s), "router"))
-        return rc;
-    if (int rc = hip_status(launch_route(logits, T, N, *params, k, ids, w, s), "route"))
-        return rc;
+    if (router_route_fusable(dtype, K)) {
+        if (int rc = hip_status(launch_router_route(x, W_router, T, d, N, *params, logits_out,
+                                                    k, ids, w, s), "router_route"))
+            return rc;
+    } else {
+        if (int rc = hip_status(launch_router(x, W_router, T, d, N, dtype, logits, s),
+                                "router"))
+            return rc;
+        if (int rc = hip_status(launch_route(logits, T, N, *params, k, ids, w, s), "route"))
+            return rc;
+    }
     return experts_impl(x, W_gate_up, W_down, k, ids, w, residual, T, d, N, m, K, dtype, y, ws,
                         L, counts_out, s);
 }

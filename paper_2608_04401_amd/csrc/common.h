@@ -53,6 +53,12 @@ hipError_t launch_dispatch(const int* k, const int* ids, int64_t T, int N, int K
 hipError_t launch_router(const void* x, const void* Wr, int64_t T, int d, int N, int dtype,
                          float* logits, hipStream_t s);
 
+// router GEMM fused with the routing (bf16, K <= kLaneMaxK); logits == nullptr: not written
+bool router_route_fusable(int dtype, int K);
+hipError_t launch_router_route(const void* x, const void* Wr, int64_t T, int d, int N,
+                               const elb_route_params& p, float* logits, int* k, int* ids,
+                               float* w, hipStream_t s);
+
 // grouped GEMMs
 // rows per M-tile of the grouped GEMMs for this problem (the dispatch scan uses the same)
 int gemm_tile_rows(int dtype, int64_t T, int K, int N, int d, int m);

@@ -1,70 +1,15 @@
-// Routing kernel: softmax, per-token descending sort, Kneedle elbow, cap, weights.
-//
-// Method (Section 2, Section 2.1 and Appendix A.1 Algorithm 1 of the paper): per token,
-// p = softmax(l); sort p in descending order; normalise the sorted curve to the unit square;
-// D_i = deviation of point i from the reference line; e = argmax D; k = min(e + 1, K).
-// The normalised curve runs from (0,0) to (1,1), as in the elbow-angle definition of
-// Section 2.3: p'_i = (p_(0) - p_(i)) / (p_(0) - p_(N-1) + eps), x'_i = i / (N - 1).
+// Routing kernel: softmax, per-token descending sort, Kneedle elbow, cap, weights (the
+// per-token arithmetic and its reading of Section 2, Section 2.1 and Appendix A.1
+// Algorithm 1 are in route_lane.h).
 //
 // GPU design (CDNA4, wave64): one LANE per token.  A wave stages its 64 tokens' logits
-// (64 * N contiguous floats) through LDS with coalesced loads, then every lane holds its
-// token's N values in registers and sorts them with a compile-time odd-even merge network
-// (all register indices are constants), so no cross-lane traffic is needed.
-//
-// Arithmetic differs from the definition only by positive scaling and the sum's
-// cancellation, which leave the argmax unchanged:
-//   u_i = exp(l_(i) - l_(0)) (so p_(i) = u_i / S, S = sum u), and
-//   D_i * (p_max - p_min + eps) * S = (1 - u_i) - x'_i * (1 - u_min + eps * S).
-// The sort key is the fp32 logit itself (softmax is strictly increasing), with ties broken
-// by the lower expert id, so the ids and their order never depend on exp/division rounding.
-#include <utility>
-
-#include "common.h"
-#include "sortnet.h"
+// (64 * N contiguous floats) through LDS with coalesced loads, then every lane routes its
+// token from its staged row.
+#include "route_lane.h"
 
 namespace elb {
 
 namespace {
-
-struct XTable {
-    float x[ELB_MAX_EXPERTS];  // x'_i = i / (N - 1), correctly rounded; x[N - 1] == 1
-};
-
-constexpr float kLog2e = 1.4426950408889634f;
-
-template <int NP>
-struct NetHolder {
-    static constexpr OddEvenMergeNet<NP> net{};
-};
-
-// Sort key of a logit: the value itself, made canonical by an add of +0 (which also turns
-// -0 into +0), so that min/max compile to single v_min_f32/v_max_f32.  Non-NaN inputs.
-__device__ __forceinline__ float order_key(float f) { return f + 0.0f; }
-
-// One comparator of the network: larger value to the lower position (v_max_f32/v_min_f32).
-template <int NP, int Q>
-__device__ __forceinline__ void compare_exchange(float* key) {
-    constexpr int a = NetHolder<NP>::net.a[Q];
-    constexpr int b = NetHolder<NP>::net.b[Q];
-    const float hi = fmaxf(key[a], key[b]);
-    const float lo = fminf(key[a], key[b]);
-    key[a] = hi;
-    key[b] = lo;
-}
-
-// The whole network as straight-line code (a fold over the comparator indices), so every
-// register index is a compile-time constant regardless of loop-unrolling heuristics.
-template <int NP, int... Q>
-__device__ __forceinline__ void sort_desc(float* key, std::integer_sequence<int, Q...>) {
-    (compare_exchange<NP, Q>(key), ...);
-}
-
-// lowest set bit of a 64-bit mask held as two 32-bit halves (0 if empty)
-__device__ __forceinline__ int lowest_bit(uint32_t lo, uint32_t hi) {
-    if (lo) return __builtin_ctz(lo);
-    if (hi) return 32 + __builtin_ctz(hi);
-    return 0;
-}
 
 // FULL: N == NP, so every "position < N" test is static; KM: a bound on K (8 or 16)
 template <int NP, bool FULL, int KMAX>
@@ -75,7 +20,6 @@ __global__ __launch_bounds__(256) void route_kernel(const float* __restrict__ lo
                                                     int* __restrict__ ids,
                                                     float* __restrict__ wout) {
     constexpr int LD = NP + 1;  // padded row: lane t reads word t*LD + c, banks (t + c) % 64
-    constexpr int KM = NP < KMAX ? NP : KMAX;
     __shared__ float lds[4 * kWave * LD];
     const int lane = threadIdx.x & (kWave - 1);
     const int wv = threadIdx.x >> 6;
@@ -87,7 +31,6 @@ __global__ __launch_bounds__(256) void route_kernel(const float* __restrict__ lo
     // ---- stage the wave's rows (contiguous in memory) through LDS, coalesced: every load
     // of the lane is issued before the first LDS write, so the wave waits for memory once ----
     const float* src = logits + t0 * N;
-    const int Nn = FULL ? NP : N;
     if (FULL && vec4) {
         constexpr int PER = NP / 4;  // float4 per lane (64 rows x NP / 4 per wave)
         const int total4 = rows * (NP / 4);
@@ -117,154 +60,15 @@ __global__ __launch_bounds__(256) void route_kernel(const float* __restrict__ lo
     }
     __syncthreads();
     if (lane >= rows) return;  // no barrier follows
-    const float* row = tile + lane * LD;
 
-    // ---- keys of the token's logits (pads are -inf and sort last) ----
-    const float kNegInf = -INFINITY;
-    float key[NP], okey[NP];
-#pragma unroll
-    for (int c = 0; c < NP; ++c) {
-        okey[c] = (c < Nn) ? order_key(row[c]) : kNegInf;
-        key[c] = okey[c];
-    }
-    sort_desc<NP>(key, std::make_integer_sequence<int, NetHolder<NP>::net.n>{});
-
-    // ---- u_i = exp(l_(i) - l_(0)) (0 for pads); S = sum u; u_min = u_(N-1) ----
-    const float lmax = key[0];
-    float u[NP];
-    float S = 0.f;
-#pragma unroll
-    for (int i = 0; i < NP; ++i) {
-        u[i] = __builtin_amdgcn_exp2f((key[i] - lmax) * kLog2e);
-        S += u[i];
-    }
-    float umin = u[NP - 1];
-    if (!FULL) {
-#pragma unroll
-        for (int i = 0; i < NP; ++i) umin = (i == Nn - 1) ? u[i] : umin;
-    }
-
-    int k = K;
-    if (mode == ELB_MODE_ELBOW) {
-        // scaled deviation (1 - u_i) - x'_i (1 - u_min + eps S); D_0 == 0 exactly.  The first
-        // argmax only matters below K - 1 (beyond it k = K), so later points need only a max.
-        // Pads have x' = +inf and never win.
-        const float Rp = (1.0f - umin) + eps * S;
-        float best = 0.f;
-        int e = 0;
-        float tail = -INFINITY;
-#pragma unroll
-        for (int i = 1; i < NP; ++i) {
-            const float Di = fmaf(-xt.x[i], Rp, 1.0f - u[i]);
-            if (i < KM - 1) {
-                const bool head = i < K - 1;
-                const bool better = head && (Di > best);  // strict: first index wins ties
-                best = better ? Di : best;
-                e = better ? i : e;
-                tail = head ? tail : fmaxf(tail, Di);
-            } else {
-                tail = fmaxf(tail, Di);
-            }
-        }
-        k = (tail > best) ? K : e + 1;
-    }
-
-    // ---- ids of the k selected experts: the k largest keys, equal keys by lower id ----
-    // tau = key of rank k-1; g = ranks < k with a key above tau; the rest of the k come
-    // from the experts whose key equals tau, lowest ids first.
-    float tau = key[0];
-    int g = 0;
-#pragma unroll
-    for (int i = 0; i < KM; ++i)
-        if (i == k - 1) tau = key[i];
-#pragma unroll
-    for (int i = 0; i < KM; ++i)
-        if (i < k && key[i] > tau) ++g;
-    // common case: exactly k experts have a key >= tau (no tie at the boundary)
-    uint32_t sel_lo = 0, sel_hi = 0;
-#pragma unroll
-    for (int c = 0; c < NP; ++c) {
-        const uint32_t bit = (c < Nn && okey[c] >= tau) ? (1u << (c & 31)) : 0u;
-        if (c < 32) sel_lo |= bit;
-        else sel_hi |= bit;
-    }
-    const bool tie = (__popc(sel_lo) + __popc(sel_hi)) != k;
-    if (__any(tie)) {  // wave-uniform slow path: ties at tau, lowest ids first
-        uint32_t eq_lo = 0, eq_hi = 0;
-        sel_lo = sel_hi = 0;
-#pragma unroll
-        for (int c = 0; c < NP; ++c) {
-            const uint32_t bit = 1u << (c & 31);
-            const bool real = c < Nn;
-            const uint32_t gt = (real && okey[c] > tau) ? bit : 0u;
-            const uint32_t eq = (real && okey[c] == tau) ? bit : 0u;
-            if (c < 32) {
-                sel_lo |= gt;
-                eq_lo |= eq;
-            } else {
-                sel_hi |= gt;
-                eq_hi |= eq;
-            }
-        }
-        for (int r = 0; r < k - g; ++r) {
-            const int b = lowest_bit(eq_lo, eq_hi);
-            if (b < 32) { sel_lo |= 1u << b; eq_lo &= ~(1u << b); }
-            else { sel_hi |= 1u << (b - 32); eq_hi &= ~(1u << (b - 32)); }
-        }
-    }
-    // the selected experts in id order, with their keys (re-read from the staged row)
-    int cid[KM];
-    float ck[KM];
-#pragma unroll
-    for (int r = 0; r < KM; ++r) {
-        const int b = lowest_bit(sel_lo, sel_hi);
-        const bool on = r < k;
-        cid[r] = b;
-        ck[r] = on ? order_key(row[b]) : -INFINITY;
-        if (b < 32) sel_lo &= sel_lo - 1;
-        else sel_hi &= sel_hi - 1;
-    }
-    // rank of each in descending order (equal keys: lower id, i.e. lower r, first)
-    const int64_t t = t0 + lane;
-    float denom = S;
-    if (renorm) {
-        float sel = 0.f;
-#pragma unroll
-        for (int j = 0; j < KM; ++j)
-            if (j < k) sel += u[j];
-        denom = sel;
-    }
-    const float inv = 1.0f / denom;
-    kout[t] = k;
-#pragma unroll
-    for (int r = 0; r < KM; ++r) {
-        if (r < k) {
-            int rank = 0;
-#pragma unroll
-            for (int q = 0; q < KM; ++q) {
-                if (q < r) rank += (q < k && ck[q] >= ck[r]) ? 1 : 0;
-                if (q > r) rank += (q < k && ck[q] > ck[r]) ? 1 : 0;
-            }
-            ids[t * K + rank] = cid[r];
-            wout[t * K + rank] =
-                __builtin_amdgcn_exp2f((ck[r] - lmax) * kLog2e) * inv;
-        }
-    }
-#pragma unroll
-    for (int j = 0; j < KM; ++j) {
-        if (j >= k && j < K) {
-            ids[t * K + j] = -1;
-            wout[t * K + j] = 0.f;
-        }
-    }
+    route_token<NP, FULL, KMAX>(tile + lane * LD, N, K, eps, mode, renorm, xt, t0 + lane, kout,
+                                ids, wout);
 }
 
 template <int NP, bool FULL, int KMAX>
 hipError_t launch_np(const float* logits, int64_t T, int N, const elb_route_params& p, int* k,
                      int* ids, float* w, hipStream_t s) {
-    XTable xt;
-    for (int i = 0; i < ELB_MAX_EXPERTS; ++i)
-        xt.x[i] = (i < N) ? (float)((double)i / (double)(N - 1)) : INFINITY;
+    const XTable xt = make_xtable(N);
     const int64_t waves = (T + kWave - 1) / kWave;
     const unsigned blocks = (unsigned)((waves + 3) / 4);
     const int vec4 = ((uintptr_t)logits % 16) == 0;

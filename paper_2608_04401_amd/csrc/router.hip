@@ -1,5 +1,5 @@
 // Router logits l = x W_r^T (Section 2: a learned router produces logits l(x) in R^N),
-// fp32 accumulation and fp32 output.
+// fp32 accumulation and fp32 output; and the router fused with the routing of its logits.
 //
 // bf16: one block of 4 waves per 16 tokens.  The 32-deep k-steps are dealt round-robin to
 // the waves, so each wave reads a distinct quarter of the 16 x d slice of x (x is read once)
@@ -8,7 +8,7 @@
 // of their use, and the 4 partial 16 x N tiles are summed in LDS in a fixed order.
 // N <= 64, d % 32 == 0.
 // fp32: one thread per (token, expert) dot product (the small fp32 configuration).
-#include "common.h"
+#include "route_lane.h"
 
 namespace elb {
 
@@ -16,13 +16,14 @@ namespace {
 
 constexpr int RW = 4;  // waves per router block
 
-__global__ __launch_bounds__(64 * RW) void router_bf16(const bf16_t* __restrict__ x,
-                                                      const bf16_t* __restrict__ Wr, int64_t T,
-                                                      int d, int N, float* __restrict__ logits) {
-    __shared__ float part[RW][16][65];  // per-wave partial logits (padded rows)
+// The 16 x N logits of tokens [t0, t0 + 16): each wave's partial sums over its k-steps go to
+// part[w] (lane rows, expert columns); the caller sums the RW partial tiles.
+__device__ __forceinline__ void router_partials(const bf16_t* __restrict__ x,
+                                                const bf16_t* __restrict__ Wr, int64_t T,
+                                                int d, int N, int64_t t0,
+                                                float (&part)[RW][16][65]) {
     const int lane = threadIdx.x & 63;
     const int w = threadIdx.x >> 6;
-    const int64_t t0 = (int64_t)blockIdx.x * 16;
     const int l16 = lane & 15;
     const int kq = (lane >> 4) * 8;
     const int64_t ta = t0 + l16;
@@ -76,24 +77,63 @@ __global__ __launch_bounds__(64 * RW) void router_bf16(const bf16_t* __restrict_
             mma(ra[p], rb[p]);
         }
     }
-
-    // sum the waves' partial tiles in a fixed order (deterministic)
     const int rq = (lane >> 4) * 4;
 #pragma unroll
     for (int g = 0; g < 4; ++g)
 #pragma unroll
         for (int r = 0; r < 4; ++r) part[w][rq + r][16 * g + l16] = acc[g][r];
+}
+
+// logit of output o of the block (token o / 64, expert o % 64): the RW partials summed in a
+// fixed order (deterministic, the same bits in every kernel that uses it)
+__device__ __forceinline__ float router_sum(const float (&part)[RW][16][65], int tr, int n) {
+    float v = part[0][tr][n];
+#pragma unroll
+    for (int ww = 1; ww < RW; ++ww) v += part[ww][tr][n];
+    return v;
+}
+
+__global__ __launch_bounds__(64 * RW) void router_bf16(const bf16_t* __restrict__ x,
+                                                      const bf16_t* __restrict__ Wr, int64_t T,
+                                                      int d, int N, float* __restrict__ logits) {
+    __shared__ float part[RW][16][65];  // per-wave partial logits (padded rows)
+    const int64_t t0 = (int64_t)blockIdx.x * 16;
+    router_partials(x, Wr, T, d, N, t0, part);
     __syncthreads();
 #pragma unroll
     for (int q = 0; q < 1024 / (64 * RW); ++q) {
-        const int o = threadIdx.x + 64 * RW * q;  // output (token o / 64, expert o % 64)
+        const int o = threadIdx.x + 64 * RW * q;
         const int tr = o >> 6, n = o & 63;
         const int64_t t = t0 + tr;
-        float v = part[0][tr][n];
-#pragma unroll
-        for (int ww = 1; ww < RW; ++ww) v += part[ww][tr][n];
-        if (t < T && n < N) logits[t * N + n] = v;
+        if (t < T && n < N) logits[t * N + n] = router_sum(part, tr, n);
     }
+}
+
+// Router GEMM and routing fused: the block's 16 x N logits are summed into LDS and routed
+// there by 16 lanes (route_token, the routing kernel's own per-token code), so the logits
+// need not travel through HBM; they are written out only when `logits` is not null.
+template <int NP, bool FULL, int KMAX>
+__global__ __launch_bounds__(64 * RW) void router_route_bf16(
+    const bf16_t* __restrict__ x, const bf16_t* __restrict__ Wr, int64_t T, int d, int N,
+    int K, float eps, int mode, int renorm, XTable xt, float* __restrict__ logits,
+    int* __restrict__ kout, int* __restrict__ ids, float* __restrict__ wout) {
+    __shared__ float part[RW][16][65];
+    const int64_t t0 = (int64_t)blockIdx.x * 16;
+    router_partials(x, Wr, T, d, N, t0, part);
+    __syncthreads();
+#pragma unroll
+    for (int q = 0; q < 1024 / (64 * RW); ++q) {
+        const int o = threadIdx.x + 64 * RW * q;
+        const int tr = o >> 6, n = o & 63;
+        const int64_t t = t0 + tr;
+        const float v = router_sum(part, tr, n);
+        part[0][tr][n] = v;  // the summed tile replaces partial 0 (same thread, same word)
+        if (logits && t < T && n < N) logits[t * N + n] = v;
+    }
+    __syncthreads();
+    if (threadIdx.x < 16 && t0 + threadIdx.x < T)
+        route_token<NP, FULL, KMAX>(&part[0][threadIdx.x][0], N, K, eps, mode, renorm, xt,
+                                    t0 + threadIdx.x, kout, ids, wout);
 }
 
 __global__ __launch_bounds__(256) void router_f32(const float* __restrict__ x,
@@ -110,7 +150,45 @@ __global__ __launch_bounds__(256) void router_f32(const float* __restrict__ x,
     logits[i] = acc;
 }
 
+template <int NP, bool FULL, int KMAX>
+void launch_rr(const void* x, const void* Wr, int64_t T, int d, int N,
+               const elb_route_params& p, float* logits, int* k, int* ids, float* w,
+               hipStream_t s) {
+    hipLaunchKernelGGL((router_route_bf16<NP, FULL, KMAX>), dim3((unsigned)((T + 15) / 16)),
+                       dim3(64 * RW), 0, s, (const bf16_t*)x, (const bf16_t*)Wr, T, d, N, p.K,
+                       p.eps, p.mode, p.renormalize, make_xtable(N), logits, k, ids, w);
+}
+
+template <int KMAX>
+void launch_rr_n(const void* x, const void* Wr, int64_t T, int d, int N,
+                 const elb_route_params& p, float* logits, int* k, int* ids, float* w,
+                 hipStream_t s) {
+    switch (N) {
+        case 8: return launch_rr<8, true, KMAX>(x, Wr, T, d, N, p, logits, k, ids, w, s);
+        case 16: return launch_rr<16, true, KMAX>(x, Wr, T, d, N, p, logits, k, ids, w, s);
+        case 32: return launch_rr<32, true, KMAX>(x, Wr, T, d, N, p, logits, k, ids, w, s);
+        case 64: return launch_rr<64, true, KMAX>(x, Wr, T, d, N, p, logits, k, ids, w, s);
+        default: break;
+    }
+    if (N < 8) return launch_rr<8, false, KMAX>(x, Wr, T, d, N, p, logits, k, ids, w, s);
+    if (N < 16) return launch_rr<16, false, KMAX>(x, Wr, T, d, N, p, logits, k, ids, w, s);
+    if (N < 32) return launch_rr<32, false, KMAX>(x, Wr, T, d, N, p, logits, k, ids, w, s);
+    return launch_rr<64, false, KMAX>(x, Wr, T, d, N, p, logits, k, ids, w, s);
+}
+
 }  // namespace
+
+bool router_route_fusable(int dtype, int K) { return dtype == ELB_BF16 && K <= kLaneMaxK; }
+
+hipError_t launch_router_route(const void* x, const void* Wr, int64_t T, int d, int N,
+                               const elb_route_params& p, float* logits, int* k, int* ids,
+                               float* w, hipStream_t s) {
+    if (T == 0) return hipSuccess;
+    ProfileScope prof("router_route_bf16", s);
+    if (p.K <= 8) launch_rr_n<8>(x, Wr, T, d, N, p, logits, k, ids, w, s);
+    else launch_rr_n<kLaneMaxK>(x, Wr, T, d, N, p, logits, k, ids, w, s);
+    return hipGetLastError();
+}
 
 hipError_t launch_router(const void* x, const void* Wr, int64_t T, int d, int N, int dtype,
                          float* logits, hipStream_t s) {

@@ -108,3 +108,15 @@ def test_dispatch_and_router_validation():
 
 def test_profile_read_empty():
     assert B.elb_profile_read() == {}
+
+
+def test_router_route_validation():
+    lib = B.lib()
+    p = B.RouteParams(8, 1e-8, 0, 0)
+    call = lambda dt=1, d=128, p=p, T=10: lib.elb_router_route(
+        DUMMY, DUMMY, T, d, 64, dt, C.byref(p), None, DUMMY, DUMMY, DUMMY, None)
+    assert call(dt=0) == UNSUPPORTED                       # fp32: use the two calls
+    assert call(p=B.RouteParams(17, 1e-8, 0, 0)) == UNSUPPORTED   # K above the lane kernel
+    assert call(d=100) == INVALID                          # bf16 router needs d % 32 == 0
+    assert call(p=B.RouteParams(8, -1.0, 0, 0)) == INVALID
+    assert call(T=0) == OK

@@ -1,0 +1,56 @@
+"""GPU: the fused router + routing kernel.  Its k, ids and w must be bit-identical to the
+two-step path (router kernel, then routing kernel) and its optional logits identical to the
+router kernel's; and, like the layer, its routing must match the oracle's on its own fp64
+logits except on near-ties."""
+import numpy as np
+import pytest
+import torch
+
+from oracle import oracle as O
+from paper_2608_04401_amd import binding as B
+from paper_2608_04401_amd import synth
+
+from helpers import NEAR_TIE, cpu, to_gpu
+
+pytestmark = pytest.mark.gpu
+BF = torch.bfloat16
+
+
+def _case(T, d, N, K, seed, **kw):
+    L = synth.moe_layer(T, d, N, 64, dtype="bf16", seed=seed)
+    x, Wr = to_gpu(L.x, BF), to_gpu(L.W_router, BF)
+    k, ids, w, lg = B.elb_router_route(x, Wr, K=K, with_logits=True, **kw)
+    lg2 = B.elb_router_logits(x, Wr)
+    k2, ids2, w2 = B.elb_route(lg2, K=K, **kw)
+    torch.cuda.synchronize()
+    assert torch.equal(lg, lg2)
+    assert torch.equal(k, k2) and torch.equal(ids, ids2) and torch.equal(w, w2)
+    # without the logits output: the same routing
+    k3, ids3, w3, none = B.elb_router_route(x, Wr, K=K, **kw)
+    torch.cuda.synchronize()
+    assert none is None and torch.equal(k3, k) and torch.equal(ids3, ids) and torch.equal(w3, w)
+    return L, k, ids, w
+
+
+@pytest.mark.parametrize("T,d,N,K", [(4096, 2048, 64, 8), (37, 96, 50, 5), (300, 320, 64, 16),
+                                     (5, 544, 3, 2), (64, 2048, 64, 8), (1, 64, 8, 8),
+                                     (1000, 128, 16, 12), (33, 256, 33, 16)])
+@pytest.mark.parametrize("mode", [B.MODE_ELBOW, B.MODE_TOPK])
+def test_fused_equals_two_step(T, d, N, K, mode):
+    _case(T, d, N, K, seed=T + d + N, mode=mode)
+
+
+@pytest.mark.parametrize("renorm", [False, True])
+@pytest.mark.parametrize("eps", [0.0, 1e-3])
+def test_fused_eps_renorm(eps, renorm):
+    _case(1000, 512, 64, 8, seed=3, eps=eps, renormalize=renorm)
+
+
+def test_fused_vs_oracle_olmoe():
+    L, k, ids, w = _case(4096, 2048, 64, 8, seed=0)
+    ref = O.route(O.router_logits(L.x, L.W_router).astype(np.float32), K=8)
+    k, ids = cpu(k), cpu(ids)
+    same = (k == ref.k) & (ids == ref.ids).all(axis=1)
+    assert (ref.margin[~same] < NEAR_TIE).all()
+    print("fused vs oracle: %d tokens, %d near-tie differences, mean k %.4f" % (
+        len(k), int((~same).sum()), k.mean()))
