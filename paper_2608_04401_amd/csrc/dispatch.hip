@@ -1,6 +1,6 @@
 // Variable-k dispatch: per-expert token lists from a routing (k_t experts per token).
 //
-// Three launches, deterministic, no atomics:
+// Three launches (one for T <= 256, dispatch_small below), deterministic, no atomics:
 //   count   one lane per token; a wave ORs each token's selected experts into a 64-bit mask
 //           and, per expert, counts the wave's tokens with one ballot + popcount.  The
 //           per-wave counts form an expert-major [N, groups] histogram.
@@ -153,11 +153,97 @@ __global__ __launch_bounds__(256) void dispatch_scatter(const int* __restrict__ 
     }
 }
 
+// Small batches (T <= 256, decode): the three steps in ONE block of 4 waves, one lane per
+// token.  The per-wave expert counts go to LDS; wave 0 turns them into per-wave bases inside
+// each expert's list and, with a wave scan over the experts, into the list and M-tile
+// offsets; then every wave places its tokens exactly as dispatch_scatter does.  Same rows,
+// same order, as the three-launch path.
+__global__ __launch_bounds__(256) void dispatch_small(const int* __restrict__ k,
+                                                      const int* __restrict__ ids, int T, int N,
+                                                      int K, int* __restrict__ counts,
+                                                      int* __restrict__ offsets,
+                                                      int* __restrict__ tile_off, int tile_rows,
+                                                      int* __restrict__ row_token,
+                                                      int* __restrict__ inv) {
+    __shared__ int base[4][kWave];  // per-wave counts, then each wave's base in the list
+    __shared__ int offs[kWave];
+    __shared__ int pos[4][kWave][kWave + 1];
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wv = threadIdx.x >> 6;
+    const int t = wv * kWave + lane;
+    const bool valid = t < T;
+    const uint64_t mask = token_mask(k, ids, t, N, K, valid);
+    int mine = 0;
+    for (int e = 0; e < N; ++e) {
+        const int c = __popcll(__ballot((mask >> e) & 1ull));
+        if (lane == e) mine = c;
+    }
+    base[wv][lane] = mine;
+    __syncthreads();
+    if (wv == 0) {
+        int c = 0;
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {  // lane e: exclusive prefix over the waves
+            const int cw = base[w][lane];
+            base[w][lane] = c;
+            c += cw;
+        }
+        if (lane >= N) c = 0;
+        const int tiles = (c + tile_rows - 1) / tile_rows;
+        int incl = c, tincl = tiles;
+        for (int dd = 1; dd < kWave; dd <<= 1) {
+            const int o = __shfl_up(incl, dd);
+            const int to = __shfl_up(tincl, dd);
+            if (lane >= dd) {
+                incl += o;
+                tincl += to;
+            }
+        }
+        offs[lane] = incl - c;
+        if (lane < N) {
+            counts[lane] = c;
+            offsets[lane] = incl - c;
+            tile_off[lane] = tincl - tiles;
+        }
+        if (lane == N - 1) {
+            offsets[N] = incl;
+            tile_off[N] = tincl;
+        }
+    }
+    __syncthreads();
+    const int base_mine = (lane < N) ? offs[lane] + base[wv][lane] : 0;
+    const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+    for (int e = 0; e < N; ++e) {
+        const bool has = (mask >> e) & 1ull;
+        const uint64_t b = __ballot(has);
+        const int bse = __shfl(base_mine, e);
+        if (has) {
+            const int r = bse + __popcll(b & below);
+            row_token[r] = t;
+            pos[wv][lane][e] = r;
+        }
+    }
+    if (!valid) return;  // no barrier follows
+    const int kt = k[t];
+    for (int j = 0; j < K; ++j) {
+        const int e = ids[(int64_t)t * K + j];
+        int r = -1;
+        if (j < kt && (unsigned)e < (unsigned)N) r = pos[wv][lane][e];
+        inv[(int64_t)t * K + j] = r;
+    }
+}
+
 }  // namespace
 
 hipError_t launch_dispatch(const int* k, const int* ids, int64_t T, int N, int K, int* counts,
                            int* offsets, int* row_token, int* inv, int* hist, int* tile_off,
                            int tile_rows, hipStream_t s) {
+    if (T <= 256) {
+        ProfileScope prof("dispatch_small", s);
+        hipLaunchKernelGGL(dispatch_small, dim3(1), dim3(256), 0, s, k, ids, (int)T, N, K,
+                           counts, offsets, tile_off, tile_rows, row_token, inv);
+        return hipGetLastError();
+    }
     const int64_t groups = dispatch_groups(T);
     // at least one scatter block, which also writes offsets and tile_off (also when T == 0)
     const unsigned blocks = (unsigned)((groups + 3) / 4 > 0 ? (groups + 3) / 4 : 1);

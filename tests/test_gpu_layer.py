@@ -29,8 +29,10 @@ def olmoe():
 
 # ------------------------------------------------------------------------------ dispatch
 @pytest.mark.parametrize("T,N,K", [(65536, 64, 8), (1000, 64, 8), (777, 5, 3), (64, 8, 8),
-                                   (1, 2, 1), (4096, 33, 16)])
+                                   (1, 2, 1), (4096, 33, 16), (256, 64, 8), (257, 64, 8),
+                                   (200, 64, 64), (130, 17, 5), (255, 3, 3)])
 def test_dispatch_matches_oracle(T, N, K):
+    """T <= 256 runs the single-block dispatch, larger T the three-launch one."""
     lg = synth.planted_logits(T, N, seed=T + N, m_max=min(8, N))
     r = O.route(lg, K=K)
     counts, offsets, row_token, inv = B.elb_dispatch(to_gpu(r.k, torch.int32),
@@ -41,6 +43,22 @@ def test_dispatch_matches_oracle(T, N, K):
     assert np.array_equal(cpu(row_token)[:len(rt0)], rt0)
     assert (cpu(row_token)[len(rt0):] == -1).all()        # rows past sum k untouched
     assert np.array_equal(cpu(inv), inv0)
+
+
+def test_dispatch_small_and_large_agree():
+    """The single-block path (T <= 256) and the three-launch path give the same lists for
+    the first 256 tokens of a routing (the three-launch run sees 300 tokens, so its first
+    256 tokens' rows precede the rest within each expert)."""
+    lg = synth.planted_logits(300, 64, seed=5)
+    r = O.route(lg, K=8)
+    k, ids = to_gpu(r.k, torch.int32), to_gpu(r.ids, torch.int32)
+    cs, os_, rts, invs = B.elb_dispatch(k[:256].contiguous(), ids[:256].contiguous(), 64)
+    cl, ol, rtl, invl = B.elb_dispatch(k, ids, 64)
+    c0, o0, rt0, inv0 = O.dispatch(r.k[:256], r.ids[:256], 64)
+    assert np.array_equal(cpu(cs), c0) and np.array_equal(cpu(rts)[:len(rt0)], rt0)
+    assert np.array_equal(cpu(invs), inv0)
+    c1, o1, rt1, inv1 = O.dispatch(r.k, r.ids, 64)
+    assert np.array_equal(cpu(cl), c1) and np.array_equal(cpu(invl), inv1)
 
 
 def test_dispatch_topk_and_ids_outside_selection():
