@@ -6,8 +6,9 @@ One step = one whole layer (router GEMM, routing, dispatch, grouped SwiGLU exper
 combine) over one batch of synthetic OLMoE-shaped tokens already resident in HBM.
 Prints ONE JSON line with tokens/s, the roofline of the dominant kernel (the grouped
 gate/up expert GEMM on MFMA), the fixed top-8 baseline through the same kernels, the
-routing kernel's HBM fraction on the routing-only workload, and the fp64 CPU oracle timed
-on a bounded token sample on this host.
+routing kernel's and the routing variants' HBM fractions on the routing-only workload, the
+decode-sized layer (T = 64) with its expert weight stream against HBM bandwidth, and the
+fp64 CPU oracle timed on a bounded token sample on this host.
 """
 from __future__ import annotations
 
@@ -120,6 +121,75 @@ def routing_only(B, torch, T=65536, N=64, K=8, nbuf=32, iters=64):
     return out
 
 
+def _profiled(B, torch, fn, iters, warm=4):
+    """Average per-kernel microseconds of `fn(i)` over `iters` calls (library hipEvents)."""
+    for i in range(warm):
+        fn(i)
+    torch.cuda.synchronize()
+    B.elb_profile_read()
+    B.elb_profile_enable(True)
+    for i in range(iters):
+        fn(i)
+    torch.cuda.synchronize()
+    B.elb_profile_enable(False)
+    return {n: v[0] / v[1] * 1e3 for n, v in B.elb_profile_read().items()}
+
+
+def routing_variants(B, torch, T=65536, N=64, K=8, nbuf=16, iters=48):
+    """The routing variants on the routing-only workload (one wave per token): tail
+    randomisation at K = 8 (draws passed in), the uncapped elbow (K = N) and the elbow angle."""
+    from paper_2608_04401_amd import synth
+    lg = torch.from_numpy(synth.planted_logits(T, N, seed=0)).cuda()
+    rd = torch.from_numpy(synth.uniform_draws(T, N, seed=0)).cuda()
+    bl = [lg.clone() for _ in range(nbuf)]
+    br = [rd.clone() for _ in range(nbuf)]
+    cases = {
+        # name: (call, algorithmic bytes: inputs read + outputs written)
+        "tail_random K=8": (lambda i: B.elb_route_tail_random(bl[i % nbuf], br[i % nbuf], K=K),
+                            2 * 4 * T * N + T * (4 + 8 * K)),
+        "uncapped K=N=64": (lambda i: B.elb_route(bl[i % nbuf], K=N),
+                            4 * T * N + T * (4 + 8 * N)),
+        "elbow_angle": (lambda i: B.elb_elbow_angle(bl[i % nbuf]), 4 * T * N + 8 * T),
+    }
+    out = {"workload": "routing-only T=%d N=%d planted logits, uniform draws" % (T, N)}
+    for name, (fn, nbytes) in cases.items():
+        us = _profiled(B, torch, fn, iters)["route_wave"]
+        gbs = nbytes / (us * 1e-6) / 1e9
+        out[name] = {"kernel": "route_wave", "us": round(us, 2), "bytes": nbytes,
+                     "GB/s": round(gbs, 1), "frac": round(gbs / PEAK_HBM_GBS, 4)}
+    return out
+
+
+def decode_layer(B, torch, synth, K=8, steps=100):
+    """The OLMoE-shaped layer at a decode batch (T = 64): latency per layer call, elbow and
+    top-8, and the weight stream of the expert GEMMs against HBM bandwidth."""
+    T, d, N, m = WORKLOADS["olmoe-decode"][:4]
+    L = synth.moe_layer(T, d, N, m, dtype="bf16", seed=0)
+    gpu = tuple(torch.from_numpy(a).to("cuda").to(torch.bfloat16)
+                for a in (L.x, L.W_router, L.W_gu, L.W_down))
+    _, dbg = B.elb_moe_forward(*gpu, K=K, debug=True)
+    torch.cuda.synchronize()
+    counts = dbg["counts"].cpu().numpy()
+    sum_k, used = int(counts.sum()), int((counts > 0).sum())
+    out = {"workload": "olmoe-decode: T=%d d_model=%d N=%d m=%d K=%d bf16" % (T, d, N, m, K),
+           "experts_used": used, "mean_k": round(sum_k / T, 4)}
+    for name, mode in (("elbow", B.MODE_ELBOW), ("topk", B.MODE_TOPK)):
+        ms, _ = time_layer(B, torch, gpu, K, mode, steps, 10, False)
+        out[name] = {"us_per_layer": round(ms * 1e3, 2), "tokens_per_s": round(T / ms * 1e3, 1)}
+    _, kern = time_layer(B, torch, gpu, K, B.MODE_ELBOW, steps, 2, True)
+    out["kernels_us"] = {n: round(v * 1e3, 2) for n, v in kern.items()}
+    g1 = next(n for n in kern if n.startswith("gemm_gate_up"))
+    g2 = next(n for n in kern if n.startswith("gemm_down"))
+    b1 = used * 2 * m * d * 2 + T * d * 2 + sum_k * m * 2
+    b2 = used * d * m * 2 + sum_k * (m + d) * 2
+    for name, kn, nb in (("gate_up", g1, b1), ("down", g2, b2)):
+        gbs = nb / (kern[kn] * 1e-3) / 1e9
+        out[name + "_weight_stream"] = {"kernel": kn, "us": round(kern[kn] * 1e3, 2),
+                                        "bytes": nb, "GB/s": round(gbs, 1),
+                                        "frac": round(gbs / PEAK_HBM_GBS, 4)}
+    return out
+
+
 def dispatch_bytes(T, N, K, sum_k):
     """Algorithmic bytes of the dispatch: reads k [T] and ids [T, K]; writes counts [N],
     offsets [N + 1], row_token [sum k] and inv [T, K] (int32)."""
@@ -209,6 +279,7 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-routing", action="store_true")
     ap.add_argument("--no-topk", action="store_true", help="skip the fixed top-K baseline")
+    ap.add_argument("--no-decode", action="store_true", help="skip the decode-sized layer")
     ap.add_argument("--counters", action="store_true",
                     help="run only the workload of the HBM-traffic counter runs")
     ap.add_argument("--traffic-from", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
@@ -356,6 +427,11 @@ def main():
     if not args.no_routing:
         log("routing-only kernel")
         res["routing_kernel"] = routing_only(B, torch)
+        log("routing variants")
+        res["routing_variants"] = routing_variants(B, torch)
+    if args.workload == "olmoe-prefill" and not args.no_decode:
+        log("decode-sized layer")
+        res["decode_layer"] = decode_layer(B, torch, synth)
     if not args.no_cpu_baseline:
         log("cpu baseline (oracle)")
         res["cpu_baseline"] = cpu_baseline(L, K)
