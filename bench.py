@@ -153,9 +153,9 @@ def routing_variants(B, torch, T=65536, N=64, K=8, nbuf=16, iters=48):
     }
     out = {"workload": "routing-only T=%d N=%d planted logits, uniform draws" % (T, N)}
     for name, (fn, nbytes) in cases.items():
-        us = _profiled(B, torch, fn, iters)["route_wave"]
+        us = _profiled(B, torch, fn, iters)["route_pair"]
         gbs = nbytes / (us * 1e-6) / 1e9
-        out[name] = {"kernel": "route_wave", "us": round(us, 2), "bytes": nbytes,
+        out[name] = {"kernel": "route_pair", "us": round(us, 2), "bytes": nbytes,
                      "GB/s": round(gbs, 1), "frac": round(gbs / PEAK_HBM_GBS, 4)}
     return out
 

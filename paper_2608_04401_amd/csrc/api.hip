@@ -233,7 +233,7 @@ int elb_route_tail_random(const float* logits, const float* rand, int64_t T, int
     if (T == 0) return ELB_OK;
     if (!logits || !rand || !k_elbow || !ids || !w)
         return fail(ELB_ERR_INVALID_ARG, "NULL tensor pointer");
-    return hip_status(launch_route_wave(logits, rand, T, N, *params, k_elbow, ids, w, nullptr,
+    return hip_status(launch_route_pair(logits, rand, T, N, *params, k_elbow, ids, w, nullptr,
                                         nullptr, (hipStream_t)stream),
                       "route_tail_random");
 }
@@ -247,7 +247,7 @@ int elb_elbow_angle(const float* logits, int64_t T, int32_t N, float eps, int32_
     if (T == 0) return ELB_OK;
     if (!logits) return fail(ELB_ERR_INVALID_ARG, "NULL tensor pointer");
     if (!e && !theta) return ELB_OK;  // nothing asked for
-    return hip_status(launch_route_wave(logits, nullptr, T, N, p, nullptr, nullptr, nullptr, e,
+    return hip_status(launch_route_pair(logits, nullptr, T, N, p, nullptr, nullptr, nullptr, e,
                                         theta, (hipStream_t)stream),
                       "elbow_angle");
 }

@@ -34,11 +34,10 @@ constexpr int kWave = 64;
 hipError_t launch_route(const float* logits, int64_t T, int N, const elb_route_params& p,
                         int* k, int* ids, float* w, hipStream_t s);
 
-// routing variants, one wave per token (caps above kLaneMaxK, tail randomisation when
-// `rand` is set, the elbow index `e` and angle `theta` when set); ids == nullptr: no
-// selection (diagnostics only)
+// routing variants (caps above kLaneMaxK, tail randomisation when `rand` is set, the elbow
+// index `e` and angle `theta` when set); ids == nullptr: no selection (diagnostics only)
 constexpr int kLaneMaxK = 16;  // largest cap of the lane-per-token routing kernel
-hipError_t launch_route_wave(const float* logits, const float* rand, int64_t T, int N,
+hipError_t launch_route_pair(const float* logits, const float* rand, int64_t T, int N,
                              const elb_route_params& p, int* k, int* ids, float* w, int* e,
                              float* theta, hipStream_t s);
 

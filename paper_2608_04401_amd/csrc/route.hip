@@ -28,36 +28,7 @@ __global__ __launch_bounds__(256) void route_kernel(const float* __restrict__ lo
     int rows = 0;
     if (t0 < T) rows = (int)((T - t0) < kWave ? (T - t0) : kWave);
 
-    // ---- stage the wave's rows (contiguous in memory) through LDS, coalesced: every load
-    // of the lane is issued before the first LDS write, so the wave waits for memory once ----
-    const float* src = logits + t0 * N;
-    if (FULL && vec4) {
-        constexpr int PER = NP / 4;  // float4 per lane (64 rows x NP / 4 per wave)
-        const int total4 = rows * (NP / 4);
-        float4 q[PER];
-#pragma unroll
-        for (int it = 0; it < PER; ++it) {
-            const int i = lane + it * kWave;
-            if (rows == kWave || i < total4) q[it] = reinterpret_cast<const float4*>(src)[i];
-        }
-        __builtin_amdgcn_sched_barrier(0);  // keep every load ahead of the first write
-#pragma unroll
-        for (int it = 0; it < PER; ++it) {
-            const int i = lane + it * kWave;
-            const int r = i / (NP / 4);
-            const int c = (i % (NP / 4)) * 4;
-            if (rows == kWave || i < total4) {
-                float* dst = tile + r * LD + c;
-                dst[0] = q[it].x; dst[1] = q[it].y; dst[2] = q[it].z; dst[3] = q[it].w;
-            }
-        }
-    } else {
-        const int total = rows * N;
-        for (int i = lane; i < total; i += kWave) {
-            const int r = i / N;
-            tile[r * LD + (i - r * N)] = src[i];
-        }
-    }
+    stage_rows<NP, FULL>(logits + t0 * N, N, rows, vec4, tile, lane);
     __syncthreads();
     if (lane >= rows) return;  // no barrier follows
 
@@ -101,7 +72,7 @@ hipError_t launch_route(const float* logits, int64_t T, int N, const elb_route_p
     if (T == 0) return hipSuccess;
     if (p.K <= 8) return launch_k<8>(logits, T, N, p, k, ids, w, s);
     if (p.K <= kLaneMaxK) return launch_k<kLaneMaxK>(logits, T, N, p, k, ids, w, s);
-    return launch_route_wave(logits, nullptr, T, N, p, k, ids, w, nullptr, nullptr, s);
+    return launch_route_pair(logits, nullptr, T, N, p, k, ids, w, nullptr, nullptr, s);
 }
 
 }  // namespace elb

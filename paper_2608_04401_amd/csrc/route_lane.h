@@ -72,6 +72,42 @@ inline XTable make_xtable(int N) {
     return xt;
 }
 
+// Stage a wave's `rows` token rows (rows * N contiguous floats at src) into its LDS tile,
+// row r at tile + r * (NP + 1), with coalesced loads: every load of the lane is issued before
+// the first LDS write, so the wave waits for memory once.  vec4: src is 16-byte aligned.
+template <int NP, bool FULL>
+__device__ __forceinline__ void stage_rows(const float* __restrict__ src, int N, int rows,
+                                           int vec4, float* tile, int lane) {
+    constexpr int LD = NP + 1;
+    if (FULL && vec4) {
+        constexpr int PER = NP / 4;  // float4 per lane (64 rows x NP / 4 per wave)
+        const int total4 = rows * (NP / 4);
+        float4 q[PER];
+#pragma unroll
+        for (int it = 0; it < PER; ++it) {
+            const int i = lane + it * kWave;
+            if (rows == kWave || i < total4) q[it] = reinterpret_cast<const float4*>(src)[i];
+        }
+        __builtin_amdgcn_sched_barrier(0);  // keep every load ahead of the first write
+#pragma unroll
+        for (int it = 0; it < PER; ++it) {
+            const int i = lane + it * kWave;
+            const int r = i / (NP / 4);
+            const int c = (i % (NP / 4)) * 4;
+            if (rows == kWave || i < total4) {
+                float* dst = tile + r * LD + c;
+                dst[0] = q[it].x; dst[1] = q[it].y; dst[2] = q[it].z; dst[3] = q[it].w;
+            }
+        }
+    } else {
+        const int total = rows * N;
+        for (int i = lane; i < total; i += kWave) {
+            const int r = i / N;
+            tile[r * LD + (i - r * N)] = src[i];
+        }
+    }
+}
+
 // Token t's routing from row[0..N) (LDS).  FULL: N == NP, so every "position < N" test is
 // static; KMAX: a bound on K (8 or 16).  Writes k[t], ids[t, 0..K), w[t, 0..K).
 template <int NP, bool FULL, int KMAX>

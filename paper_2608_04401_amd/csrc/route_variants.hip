@@ -1,146 +1,249 @@
-// Routing variants: one WAVE per token, one lane per expert.
+// Routing variants (Section 2.1, 2.2, 2.3): caps above 16 up to N (the uncapped elbow
+// routing is K = N), tail randomisation (the experts after the elbow replaced by experts
+// drawn from outside the elbow's selection) and the elbow angle with the uncapped elbow
+// index.
 //
-// Serves what the lane-per-token routing kernel does not: caps above 16 up to N (the
-// uncapped "Elbow-N" routing is K = N), tail randomisation (Section 2.2: the experts after
-// the elbow are replaced by experts drawn from outside the elbow's selection) and the elbow
-// angle of Section 2.3.  Every lane knows its expert's exact rank in the order (logit
-// descending, expert id ascending) -- the number of experts ahead of it, counted against
-// the 64 logits broadcast one by one -- so the whole permutation is available and each
-// output is written by the lane that owns it.
-//
-// Same arithmetic as the main routing kernel: u_i = exp(l_(i) - l_(0)), S = sum u, and the
-// scaled deviation D_i = (1 - u_i) - x'_i (1 - u_min + eps S), whose first argmax over all
-// ranks is the elbow index e (the definition's D times the positive (p_max - p_min + eps) S).
-// The elbow point is (x'_e, p'_e) with p'_e = (1 - u_e) / (1 - u_min + eps S).
-#include "common.h"
+// One LANE per token with the routing kernel's staging and arithmetic (route_lane.h), but the
+// sorting network carries the expert ids along with the logits, so the id at every rank is
+// known and any cap up to N costs the same.  Same bits as the routing kernel: the same keys,
+// u_i = exp(l_(i) - l_(0)) in rank order, S summed in rank order, the same scaled deviation
+// and first argmax, w = u * (1 / denominator).
+#include "route_lane.h"
 
 namespace elb {
 
 namespace {
 
-constexpr float kLog2eV = 1.4426950408889634f;
+// ---------------------------------------------------------------------------------------
+// One LANE per token, (key, id) pairs sorted by a network: the same staging and arithmetic as
+// the routing kernel, but the sort carries the expert ids, so every rank's id is known and
+// any cap up to N costs no more than K = 1.  A pair is one 64-bit integer: the logit's
+// order-preserving integer image in the high word and (NP - 1 - id) in the low word, so one
+// signed 64-bit comparison orders by logit descending, then id ascending (pads, -inf with the
+// largest ids, sort last).  Each comparator is one v_cmp_gt_i64 and four v_cndmask_b32.
+// ---------------------------------------------------------------------------------------
 
-__device__ __forceinline__ float wave_sum(float x) {
-#pragma unroll
-    for (int o = 1; o < kWave; o <<= 1) x += __shfl_xor(x, o);
-    return x;  // every lane: the same bits (each step adds two equal-order partial sums)
+// order-preserving signed integer image of a canonical (non-NaN, no -0) fp32 value; its
+// own inverse
+__device__ __forceinline__ int ord_flip(int i) { return i ^ ((i >> 31) & 0x7fffffff); }
+
+template <int NP, int Q>
+__device__ __forceinline__ void cx_pair(int64_t* v) {
+    constexpr int a = NetHolder<NP>::net.a[Q];
+    constexpr int b = NetHolder<NP>::net.b[Q];
+    const bool sw = v[b] > v[a];
+    const int64_t hi = sw ? v[b] : v[a];
+    const int64_t lo = sw ? v[a] : v[b];
+    v[a] = hi;
+    v[b] = lo;
+}
+template <int NP, int... Q>
+__device__ __forceinline__ void sort_pairs_desc(int64_t* v, std::integer_sequence<int, Q...>) {
+    (cx_pair<NP, Q>(v), ...);
 }
 
-// (value, index) pair reductions over the wave; ties: lower index
-__device__ __forceinline__ void wave_argmax(float& v, int& i) {
-#pragma unroll
-    for (int o = 1; o < kWave; o <<= 1) {
-        const float pv = __shfl_xor(v, o);
-        const int pi = __shfl_xor(i, o);
-        const bool take = pv > v || (pv == v && pi < i);
-        v = take ? pv : v;
-        i = take ? pi : i;
-    }
-}
-__device__ __forceinline__ void wave_argmin(float& v, int& i) {
-#pragma unroll
-    for (int o = 1; o < kWave; o <<= 1) {
-        const float pv = __shfl_xor(v, o);
-        const int pi = __shfl_xor(i, o);
-        const bool take = pv < v || (pv == v && pi < i);
-        v = take ? pv : v;
-        i = take ? pi : i;
-    }
-}
-
-// value of lane `src` (wave-uniform)
-__device__ __forceinline__ float lane_value(float x, int src) {
-    return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, x), src));
-}
-
-// first lane whose predicate holds (0 if none, which finite inputs never give)
-__device__ __forceinline__ int first_lane(bool pred) {
-    const uint64_t b = __ballot(pred);
-    return b ? __builtin_ctzll(b) : 0;
-}
-
-__global__ __launch_bounds__(256) void route_wave_kernel(
+template <int NP, bool FULL>
+__global__ __launch_bounds__(256) void route_pair_kernel(
     const float* __restrict__ logits, const float* __restrict__ rand, int64_t T, int N, int K,
-    float eps, int mode, int renorm, int* __restrict__ kout, int* __restrict__ ids,
-    float* __restrict__ wout, int* __restrict__ eout, float* __restrict__ thout) {
+    float eps, int mode, int renorm, int vec4, XTable xt, int* __restrict__ kout,
+    int* __restrict__ ids, float* __restrict__ wout, int* __restrict__ eout,
+    float* __restrict__ thout) {
+    constexpr int LD = NP + 1;
+    __shared__ float lds[4 * kWave * LD];
     const int lane = threadIdx.x & (kWave - 1);
-    const int64_t t = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-    if (t >= T) return;  // wave-uniform; no barriers in this kernel
-    const bool real = lane < N;
-    // canonical key (x + 0 turns -0 into +0); pads sort last
-    const float key = real ? logits[t * N + lane] + 0.0f : -INFINITY;
+    const int wv = threadIdx.x >> 6;
+    const int64_t t0 = ((int64_t)blockIdx.x * 4 + wv) * kWave;
+    float* tile = lds + wv * kWave * LD;
+    int rows = 0;
+    if (t0 < T) rows = (int)((T - t0) < kWave ? (T - t0) : kWave);
+    stage_rows<NP, FULL>(logits + t0 * N, N, rows, vec4, tile, lane);
+    __syncthreads();
+    // lanes past the last token route a copy of the first one and write nothing: every lane
+    // takes part in the staged stores at the end (no barrier follows)
+    const bool active = lane < rows;
+    const float* row = tile + (active ? lane : 0) * LD;
+    const int64_t t = t0 + (active ? lane : 0);
+    const int Nn = FULL ? NP : N;
 
-    // rank of this expert in (key descending, id ascending)
-    int rank = 0;
-    for (int q = 0; q < N; ++q) {
-        const float kq = lane_value(key, q);
-        rank += (kq > key || (kq == key && q < lane)) ? 1 : 0;
+    // ---- sort (key, id) pairs: rank r holds key[r] and id[r] ----
+    int64_t v[NP];
+#pragma unroll
+    for (int c = 0; c < NP; ++c) {
+        const float f = (c < Nn) ? order_key(row[c]) : -INFINITY;
+        v[c] = ((int64_t)ord_flip(__float_as_int(f)) << 32) | (uint32_t)(NP - 1 - c);
     }
-    if (!real) rank = kWave;  // never selected, never the elbow
+    sort_pairs_desc<NP>(v, std::make_integer_sequence<int, NetHolder<NP>::net.n>{});
+    float key[NP];
+    int id[NP];
+#pragma unroll
+    for (int r = 0; r < NP; ++r) {
+        key[r] = __int_as_float(ord_flip((int)(v[r] >> 32)));
+        id[r] = NP - 1 - (int)(uint32_t)v[r];
+    }
 
-    // u = exp(l - l_(0)); S; u_min = u of rank N - 1
-    const float lmax = lane_value(key, first_lane(rank == 0));
-    const float u = real ? __builtin_amdgcn_exp2f((key - lmax) * kLog2eV) : 0.f;
-    const float S = wave_sum(u);
-    const float umin = lane_value(u, first_lane(rank == N - 1));
+    // ---- u, S, u_min and the elbow: the routing kernel's arithmetic, in rank order ----
+    const float lmax = key[0];
+    float u[NP];
+    float S = 0.f;
+#pragma unroll
+    for (int i = 0; i < NP; ++i) {
+        u[i] = __builtin_amdgcn_exp2f((key[i] - lmax) * kLog2e);
+        S += u[i];
+    }
+    float umin = u[NP - 1];
+    if (!FULL) {
+#pragma unroll
+        for (int i = 0; i < NP; ++i) umin = (i == Nn - 1) ? u[i] : umin;
+    }
     const float Rp = (1.0f - umin) + eps * S;
-    const float xr = real ? (float)((double)rank / (double)(N - 1)) : INFINITY;
-    // elbow: first argmax over the ranks of the scaled deviation (D_0 == 0 exactly)
-    float D = real ? fmaf(-xr, Rp, 1.0f - u) : -INFINITY;
-    int e = real ? rank : kWave;
-    wave_argmax(D, e);
-    const int k = (mode == ELB_MODE_TOPK) ? K : (e + 1 < K ? e + 1 : K);
-
-    if (eout && lane == 0) eout[t] = e;
-    if (thout && rank == e) {  // the elbow's lane: angle between (0,0), the point, (1,1)
-        float th = 180.0f;  // no point below the chord: e = 0, taken as a straight line
+    float best = 0.f;  // D_0 == 0 exactly
+    int e = 0;
+#pragma unroll
+    for (int i = 1; i < NP; ++i) {
+        const float Di = fmaf(-xt.x[i], Rp, 1.0f - u[i]);  // pads: x' = +inf, never win
+        const bool better = Di > best;  // strict: the first index wins ties
+        best = better ? Di : best;
+        e = better ? i : e;
+    }
+    if (eout && active) eout[t] = e;
+    if (thout && active) {  // the angle at the elbow point (x'_e, p'_e) between (0,0) and (1,1)
+        float th = 180.0f;  // e = 0: no point off the chord, a straight curve
         if (e > 0) {
-            // atan2(|v1 x v2|, v1 . v2): well conditioned near 90 and 180 degrees, unlike acos
-            const float pe = (1.0f - u) / Rp;
-            const float v1x = -xr, v1y = -pe, v2x = 1.0f - xr, v2y = 1.0f - pe;
+            float xe = 0.f, ue = 0.f;
+#pragma unroll
+            for (int i = 1; i < NP; ++i) {
+                xe = (i == e) ? xt.x[i] : xe;
+                ue = (i == e) ? u[i] : ue;
+            }
+            const float pe = (1.0f - ue) / Rp;
+            const float v1x = -xe, v1y = -pe, v2x = 1.0f - xe, v2y = 1.0f - pe;
             const float dot = fmaf(v1x, v2x, v1y * v2y);
             const float crs = fmaf(v1x, v2y, -(v1y * v2x));
             th = atan2f(fabsf(crs), dot) * (180.0f / 3.14159265358979323846f);
         }
         thout[t] = th;
     }
-    if (kout && lane == 0) kout[t] = k;
     if (!ids) return;
+    const int k = (mode == ELB_MODE_TOPK) ? K : (e + 1 < K ? e + 1 : K);
+    if (active) kout[t] = k;
 
-    // selection: ranks < k, then (tail randomisation) K - k experts from outside them,
-    // those with the smallest draws in increasing order (ties: lower id)
-    const bool sel = real && rank < k;
-    int slot = sel ? rank : -1;
     if (rand) {
-        const float draw = real ? rand[t * N + lane] : INFINITY;
-        for (int j = k; j < K; ++j) {
-            float v = (real && slot < 0) ? draw : INFINITY;
-            int who = (real && slot < 0) ? lane : kWave;
-            wave_argmin(v, who);
-            if (lane == who) slot = j;
+        // tail randomisation: K - k experts outside the first k ranks, smallest draws first
+        // (equal draws: lower id); weights are the experts' own probabilities
+        const float* rr = rand + t * N;
+        float draw[NP];
+#pragma unroll
+        for (int c = 0; c < NP; ++c) draw[c] = (c < Nn) ? rr[c] : INFINITY;
+        uint64_t taken = 0;
+#pragma unroll
+        for (int r = 0; r < NP; ++r)
+            if (r < k) taken |= 1ull << id[r];
+
+        float denom = S;
+        if (renorm) {
+            denom = 0.f;
+#pragma unroll
+            for (int j = 0; j < NP; ++j)
+                if (j < k) denom += u[j];
         }
+        // pass 1: the tail's ids, with unnormalised weights u (the denominator needs them all)
+        for (int j = k; j < K; ++j) {
+            float bv = INFINITY;
+            int bc = -1;
+#pragma unroll
+            for (int c = 0; c < NP; ++c) {
+                const bool ok = c < Nn && !((taken >> c) & 1ull) && (bc < 0 || draw[c] < bv);
+                bv = ok ? draw[c] : bv;
+                bc = ok ? c : bc;
+            }
+            taken |= 1ull << bc;
+            const float ub = __builtin_amdgcn_exp2f((order_key(row[bc]) - lmax) * kLog2e);
+            if (active) {
+                ids[t * K + j] = bc;
+                wout[t * K + j] = ub;
+            }
+            if (renorm) denom += ub;
+        }
+        const float inv = 1.0f / denom;
+        if (!active) return;
+#pragma unroll
+        for (int r = 0; r < NP; ++r) {
+            if (r < k) {
+                ids[t * K + r] = id[r];
+                wout[t * K + r] = u[r] * inv;
+            }
+        }
+        for (int j = k; j < K; ++j) wout[t * K + j] *= inv;  // pass 2 (this lane's own writes)
+        return;
     }
     float denom = S;
-    if (renorm) denom = wave_sum(slot >= 0 ? u : 0.f);
-    if (slot >= 0) {
-        ids[t * K + slot] = lane;
-        wout[t * K + slot] = u / denom;
+    if (renorm) {
+        float sel = 0.f;
+#pragma unroll
+        for (int j = 0; j < NP; ++j)
+            if (j < k) sel += u[j];
+        denom = sel;
     }
-    if (!rand && lane >= k && lane < K) {  // empty slots
-        ids[t * K + lane] = -1;
-        wout[t * K + lane] = 0.f;
+    const float inv = 1.0f / denom;
+    if (K <= 16) {  // few slots: direct stores
+        if (!active) return;
+#pragma unroll
+        for (int r = 0; r < NP; ++r) {
+            if (r < k) {
+                ids[t * K + r] = id[r];
+                wout[t * K + r] = u[r] * inv;
+            } else if (r < K) {
+                ids[t * K + r] = -1;
+                wout[t * K + r] = 0.f;
+            }
+        }
+        return;
     }
+    // many slots: stage the wave's 64 output rows in its LDS tile (its logits have been read;
+    // a wave's LDS operations complete in order), rows padded to K + 1 words, then store each
+    // token's K contiguous values with the whole wave
+    int* sti = reinterpret_cast<int*>(tile);
+#pragma unroll
+    for (int r = 0; r < NP; ++r)
+        if (r < K) sti[lane * (K + 1) + r] = (r < k) ? id[r] : -1;
+    for (int q = 0; q < rows; ++q)
+        for (int c = lane; c < K; c += kWave) ids[(t0 + q) * K + c] = sti[q * (K + 1) + c];
+#pragma unroll
+    for (int r = 0; r < NP; ++r)
+        if (r < K) tile[lane * (K + 1) + r] = (r < k) ? u[r] * inv : 0.f;
+    for (int q = 0; q < rows; ++q)
+        for (int c = lane; c < K; c += kWave) wout[(t0 + q) * K + c] = tile[q * (K + 1) + c];
+}
+
+template <int NP, bool FULL>
+void launch_pair_np(const float* logits, const float* rand, int64_t T, int N,
+                    const elb_route_params& p, int* k, int* ids, float* w, int* e, float* theta,
+                    hipStream_t s) {
+    const int64_t waves = (T + kWave - 1) / kWave;
+    const int vec4 = ((uintptr_t)logits % 16) == 0;
+    hipLaunchKernelGGL((route_pair_kernel<NP, FULL>), dim3((unsigned)((waves + 3) / 4)),
+                       dim3(256), 0, s, logits, rand, T, N, p.K, p.eps, p.mode, p.renormalize,
+                       vec4, make_xtable(N), k, ids, w, e, theta);
 }
 
 }  // namespace
 
-hipError_t launch_route_wave(const float* logits, const float* rand, int64_t T, int N,
+hipError_t launch_route_pair(const float* logits, const float* rand, int64_t T, int N,
                              const elb_route_params& p, int* k, int* ids, float* w, int* e,
                              float* theta, hipStream_t s) {
     if (T == 0) return hipSuccess;
-    ProfileScope prof("route_wave", s);
-    hipLaunchKernelGGL(route_wave_kernel, dim3((unsigned)((T + 3) / 4)), dim3(256), 0, s, logits,
-                       rand, T, N, p.K, p.eps, p.mode, p.renormalize, k, ids, w, e, theta);
+    ProfileScope prof("route_pair", s);
+    switch (N) {
+        case 8: launch_pair_np<8, true>(logits, rand, T, N, p, k, ids, w, e, theta, s); break;
+        case 16: launch_pair_np<16, true>(logits, rand, T, N, p, k, ids, w, e, theta, s); break;
+        case 32: launch_pair_np<32, true>(logits, rand, T, N, p, k, ids, w, e, theta, s); break;
+        case 64: launch_pair_np<64, true>(logits, rand, T, N, p, k, ids, w, e, theta, s); break;
+        default:
+            if (N < 8) launch_pair_np<8, false>(logits, rand, T, N, p, k, ids, w, e, theta, s);
+            else if (N < 16) launch_pair_np<16, false>(logits, rand, T, N, p, k, ids, w, e, theta, s);
+            else if (N < 32) launch_pair_np<32, false>(logits, rand, T, N, p, k, ids, w, e, theta, s);
+            else launch_pair_np<64, false>(logits, rand, T, N, p, k, ids, w, e, theta, s);
+    }
     return hipGetLastError();
 }
 
