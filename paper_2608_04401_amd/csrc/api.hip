@@ -54,7 +54,7 @@ Layout layout(int64_t T, int d, int N, int m, int K, int dtype) {
     };
     const size_t rows = (size_t)T * K;
     L.hist = take((size_t)dispatch_groups(T) * N * 4);
-    L.tile_off = take((size_t)(N + 1) * 4);
+    L.tile_off = take((size_t)(N + 1 + kTailMax + 1) * 4);  // tile_off, then tail_list
     L.counts = take((size_t)N * 4);
     L.offsets = take((size_t)(N + 1) * 4);
     L.row_token = take(rows * 4);
@@ -68,6 +68,21 @@ Layout layout(int64_t T, int d, int N, int m, int K, int dtype) {
     L.w = take(rows * 4);
     L.total = o;
     return L;
+}
+
+// compute units of the current device (cached; at least 1)
+int cus_per_device() {
+    static std::atomic<int> cache[64];
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+    int v = cache[dev].load();
+    if (v == 0) {
+        if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+            v < 1)
+            v = 256;
+        cache[dev].store(v);
+    }
+    return v;
 }
 
 int64_t max_tiles(int64_t T, int K, int N, int tile_rows) {
@@ -254,7 +269,8 @@ int elb_elbow_angle(const float* logits, int64_t T, int32_t N, float eps, int32_
 
 size_t elb_dispatch_workspace_bytes(int64_t T, int32_t N) {
     if (T < 0 || N < 1) return 0;
-    return align_up((size_t)dispatch_groups(T) * N * 4) + align_up((size_t)(N + 1) * 4);
+    return align_up((size_t)dispatch_groups(T) * N * 4) +
+           align_up((size_t)(N + 1 + kTailMax + 1) * 4);
 }
 
 int elb_dispatch(const int32_t* k, const int32_t* ids, int64_t T, int32_t N, int32_t K,
@@ -276,8 +292,9 @@ int elb_dispatch(const int32_t* k, const int32_t* ids, int64_t T, int32_t N, int
     char* ws = (char*)workspace;
     int* hist = (int*)ws;
     int* tile_off = (int*)(ws + align_up((size_t)dispatch_groups(T) * N * 4));
+    const TilePlan plan{128, 0, 1, kTailMax};  // plain ceil(c / 128) tiles, no tail list use
     return hip_status(launch_dispatch(k, ids, T, N, K, counts, offsets, row_token, inv, hist,
-                                      tile_off, 128, (hipStream_t)stream),
+                                      tile_off, tile_off + N + 1, plan, (hipStream_t)stream),
                       "dispatch");
 }
 
@@ -303,8 +320,14 @@ static int experts_impl(const void* x, const void* W_gate_up, const void* W_down
     void* Y = ws + L.Y;
     const int tr = gemm_tile_rows(dtype, T, K, N, d, m);
     const int64_t mt = max_tiles(T, K, N, tr);
+    int* tail_list = tile_off + N + 1;
+    // the large-tile kernel (256-row tiles, m / 128 tiles across per M-tile, one block per
+    // CU) leaves short remainders to the tail kernel when that saves a round of blocks
+    const bool big = (dtype == ELB_BF16 && tr == 256);
+    const TilePlan plan{tr, big ? kTailRows : 0, big ? cus_per_device() / (m / 128) : 1,
+                        kTailMax};
     if (int rc = hip_status(launch_dispatch(k, ids, T, N, K, counts, offsets, row_token, inv,
-                                            hist, tile_off, tr, s), "dispatch"))
+                                            hist, tile_off, tail_list, plan, s), "dispatch"))
         return rc;
     if (gemm_use_skinny(dtype, T, K, N, d, m)) {
         if (int rc = hip_status(launch_gemm_skinny(x, W_gate_up, W_down, row_token, offsets, d,
@@ -312,11 +335,14 @@ static int experts_impl(const void* x, const void* W_gate_up, const void* W_down
             return rc;
     } else {
         if (int rc = hip_status(launch_gemm_gate_up(x, W_gate_up, row_token, offsets, tile_off,
-                                                    mt, tr, d, N, m, dtype, H, s),
+                                                    big ? tail_list : nullptr, mt, tr, d, N, m,
+                                                    dtype, H, s),
                                 "gemm_gate_up"))
             return rc;
-        if (int rc = hip_status(launch_gemm_down(H, W_down, offsets, tile_off, mt, tr, d, N, m,
-                                                 dtype, Y, s), "gemm_down"))
+        if (int rc = hip_status(launch_gemm_down(H, W_down, offsets, tile_off,
+                                                 big ? tail_list : nullptr, mt, tr, d, N, m,
+                                                 dtype, Y, s),
+                                "gemm_down"))
             return rc;
     }
     return hip_status(launch_combine(Y, k, inv, w, residual, T, d, K, dtype, y, s), "combine");

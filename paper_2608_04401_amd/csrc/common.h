@@ -43,10 +43,25 @@ hipError_t launch_route_pair(const float* logits, const float* rand, int64_t T, 
 
 // dispatch: number of 64-token groups and the workspace it needs
 inline int64_t dispatch_groups(int64_t T) { return (T + kWave - 1) / kWave; }
-// hist [groups, N] int32 scratch; tile_off [N + 1] (tiles of `tile_rows` rows per expert)
+
+// M-tiling of the grouped GEMMs, computed by the dispatch on the device from the counts.
+// Each expert gets ceil(c / tile_rows) M-tiles, except that with tail_rows > 0 an expert with
+// at least one full tile and a remainder of at most tail_rows rows may leave that remainder to
+// the tail kernel (listed in tail_list: count, then expert ids) -- done only when it lowers
+// the number of rounds of tiles_per_round M-tiles and at most tail_max experts are concerned.
+struct TilePlan {
+    int tile_rows;
+    int tail_rows;
+    int tiles_per_round;
+    int tail_max;
+};
+constexpr int kTailMax = 16;   // most experts whose remainders go to the tail kernel
+constexpr int kTailRows = 32;  // largest remainder the tail kernel takes
+
+// hist [groups, N] int32 scratch; tile_off [N + 1]; tail_list [kTailMax + 1]
 hipError_t launch_dispatch(const int* k, const int* ids, int64_t T, int N, int K, int* counts,
                            int* offsets, int* row_token, int* inv, int* hist, int* tile_off,
-                           int tile_rows, hipStream_t s);
+                           int* tail_list, const TilePlan& plan, hipStream_t s);
 
 // router logits
 hipError_t launch_router(const void* x, const void* Wr, int64_t T, int d, int N, int dtype,
@@ -61,13 +76,16 @@ hipError_t launch_router_route(const void* x, const void* Wr, int64_t T, int d, 
 // grouped GEMMs
 // rows per M-tile of the grouped GEMMs for this problem (the dispatch scan uses the same)
 int gemm_tile_rows(int dtype, int64_t T, int K, int N, int d, int m);
+// tail_list (large-tile kernels only, TilePlan): its experts' remainder rows are computed
+// by extra blocks of the same launch
 hipError_t launch_gemm_gate_up(const void* x, const void* Wgu, const int* row_token,
-                               const int* offsets, const int* tile_off, int64_t max_tiles,
-                               int tile_rows, int d, int N, int m, int dtype, void* H,
-                               hipStream_t s);
+                               const int* offsets, const int* tile_off, const int* tail_list,
+                               int64_t max_tiles, int tile_rows, int d, int N, int m,
+                               int dtype, void* H, hipStream_t s);
 hipError_t launch_gemm_down(const void* H, const void* Wd, const int* offsets,
-                            const int* tile_off, int64_t max_tiles, int tile_rows, int d, int N,
-                            int m, int dtype, void* Y, hipStream_t s);
+                            const int* tile_off, const int* tail_list, int64_t max_tiles,
+                            int tile_rows, int d, int N, int m, int dtype, void* Y,
+                            hipStream_t s);
 
 // decode-sized batches: weight-streaming gate/up (+SwiGLU) and down GEMMs, both launched
 bool gemm_use_skinny(int dtype, int64_t T, int K, int N, int d, int m);

@@ -33,6 +33,37 @@ __device__ __forceinline__ uint64_t token_mask(const int* __restrict__ k,
     return mask;
 }
 
+// The M-tile count of expert `lane` (c rows) under the plan; on the whole wave (lane e < N
+// holds expert e), so that the tail decision sees every expert.  tail_mine: the expert's
+// remainder goes to the tail kernel; n_tail: how many experts do.
+__device__ __forceinline__ int plan_tiles(int c, int lane, int N, const TilePlan& tp,
+                                          bool& tail_mine, int& n_tail) {
+    const int full = c / tp.tile_rows;
+    const int rem = c - full * tp.tile_rows;
+    const int tiles = full + (rem > 0 ? 1 : 0);
+    const bool cand = tp.tail_rows > 0 && lane < N && full >= 1 && rem > 0 &&
+                      rem <= tp.tail_rows;
+    int sum = lane < N ? tiles : 0;
+#pragma unroll
+    for (int o = 1; o < kWave; o <<= 1) sum += __shfl_xor(sum, o);
+    const int nc = __popcll(__ballot(cand));
+    const int r_all = (sum + tp.tiles_per_round - 1) / tp.tiles_per_round;
+    const int r_tail = (sum - nc + tp.tiles_per_round - 1) / tp.tiles_per_round;
+    const bool use = nc > 0 && nc <= tp.tail_max && r_tail < r_all;
+    tail_mine = use && cand;
+    n_tail = use ? nc : 0;
+    return tail_mine ? full : tiles;
+}
+
+// the compact list of tail experts (by wave 0 of block 0)
+__device__ __forceinline__ void write_tail_list(bool tail_mine, int n_tail, int lane,
+                                                int* __restrict__ tail_list) {
+    const uint64_t b = __ballot(tail_mine);
+    const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+    if (tail_mine) tail_list[1 + __popcll(b & below)] = lane;
+    if (lane == 0) tail_list[0] = n_tail;
+}
+
 __global__ __launch_bounds__(256) void dispatch_count(const int* __restrict__ k,
                                                       const int* __restrict__ ids, int64_t T,
                                                       int N, int K, int* __restrict__ hist) {
@@ -95,7 +126,8 @@ __global__ __launch_bounds__(256) void dispatch_scatter(const int* __restrict__ 
                                                         const int* __restrict__ counts,
                                                         int* __restrict__ offsets,
                                                         int* __restrict__ tile_off,
-                                                        int tile_rows,
+                                                        int* __restrict__ tail_list,
+                                                        TilePlan plan,
                                                         int* __restrict__ row_token,
                                                         int* __restrict__ inv) {
     __shared__ int pos[4][kWave][kWave + 1];
@@ -106,7 +138,9 @@ __global__ __launch_bounds__(256) void dispatch_scatter(const int* __restrict__ 
     const int64_t groups = (T + kWave - 1) / kWave;
     // expert list offsets and M-tile offsets: exclusive prefixes over the experts (lane e)
     const int c = (lane < N) ? counts[lane] : 0;
-    const int tiles = (c + tile_rows - 1) / tile_rows;
+    bool tail_mine;
+    int n_tail;
+    const int tiles = plan_tiles(c, lane, N, plan, tail_mine, n_tail);  // whole wave
     int incl = c, tincl = tiles;
     for (int dd = 1; dd < kWave; dd <<= 1) {
         const int o = __shfl_up(incl, dd);
@@ -126,6 +160,7 @@ __global__ __launch_bounds__(256) void dispatch_scatter(const int* __restrict__ 
             offsets[N] = incl;
             tile_off[N] = tincl;
         }
+        write_tail_list(tail_mine, n_tail, lane, tail_list);
     }
     if (g >= groups) return;  // wave-uniform; no block barrier in this kernel
     const bool valid = t < T;
@@ -162,7 +197,9 @@ __global__ __launch_bounds__(256) void dispatch_small(const int* __restrict__ k,
                                                       const int* __restrict__ ids, int T, int N,
                                                       int K, int* __restrict__ counts,
                                                       int* __restrict__ offsets,
-                                                      int* __restrict__ tile_off, int tile_rows,
+                                                      int* __restrict__ tile_off,
+                                                      int* __restrict__ tail_list,
+                                                      TilePlan plan,
                                                       int* __restrict__ row_token,
                                                       int* __restrict__ inv) {
     __shared__ int base[4][kWave];  // per-wave counts, then each wave's base in the list
@@ -189,7 +226,9 @@ __global__ __launch_bounds__(256) void dispatch_small(const int* __restrict__ k,
             c += cw;
         }
         if (lane >= N) c = 0;
-        const int tiles = (c + tile_rows - 1) / tile_rows;
+        bool tail_mine;
+        int n_tail;
+        const int tiles = plan_tiles(c, lane, N, plan, tail_mine, n_tail);
         int incl = c, tincl = tiles;
         for (int dd = 1; dd < kWave; dd <<= 1) {
             const int o = __shfl_up(incl, dd);
@@ -209,6 +248,7 @@ __global__ __launch_bounds__(256) void dispatch_small(const int* __restrict__ k,
             offsets[N] = incl;
             tile_off[N] = tincl;
         }
+        write_tail_list(tail_mine, n_tail, lane, tail_list);
     }
     __syncthreads();
     const int base_mine = (lane < N) ? offs[lane] + base[wv][lane] : 0;
@@ -237,11 +277,11 @@ __global__ __launch_bounds__(256) void dispatch_small(const int* __restrict__ k,
 
 hipError_t launch_dispatch(const int* k, const int* ids, int64_t T, int N, int K, int* counts,
                            int* offsets, int* row_token, int* inv, int* hist, int* tile_off,
-                           int tile_rows, hipStream_t s) {
+                           int* tail_list, const TilePlan& plan, hipStream_t s) {
     if (T <= 256) {
         ProfileScope prof("dispatch_small", s);
         hipLaunchKernelGGL(dispatch_small, dim3(1), dim3(256), 0, s, k, ids, (int)T, N, K,
-                           counts, offsets, tile_off, tile_rows, row_token, inv);
+                           counts, offsets, tile_off, tail_list, plan, row_token, inv);
         return hipGetLastError();
     }
     const int64_t groups = dispatch_groups(T);
@@ -261,7 +301,7 @@ hipError_t launch_dispatch(const int* k, const int* ids, int64_t T, int N, int K
     {
         ProfileScope prof("dispatch_scatter", s);
         hipLaunchKernelGGL(dispatch_scatter, dim3(blocks), dim3(256), 0, s, k, ids, T, N, K,
-                           hist, counts, offsets, tile_off, tile_rows, row_token, inv);
+                           hist, counts, offsets, tile_off, tail_list, plan, row_token, inv);
     }
     return hipGetLastError();
 }

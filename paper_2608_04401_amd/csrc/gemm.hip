@@ -15,7 +15,7 @@
 // banks.  In gate_up the 128 B-tile columns are 64 gate and the matching 64 up columns, and
 // each wave owns matching gate/up 16-column pairs, so SwiGLU is applied in registers.
 // fp32 path: plain VALU FMA tiles (64 x 64 x 16), for the fp32 configuration.
-#include "common.h"
+#include "gemm_stream.h"
 
 namespace elb {
 
@@ -255,11 +255,77 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
     return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2_vt));
 }
 
+// Remainder rows of the large-tile GEMM (TilePlan): for each expert e in tail_list, the
+// 1..kTailRows rows past its last full M-tile, by extra blocks at the end of the grid, one per
+// (listed expert, task) of gemm_stream.h.  The 4 waves split the contraction's 64-deep stages
+// four ways; the partial tiles are summed in LDS in a fixed order and wave 0 stores them.
+template <int MODE, int MT>
+__device__ __forceinline__ void tail_task(const bf16_t* const (&wp)[SK_NF],
+                                          const bf16_t* const (&xp)[2], int s0, int s1,
+                                          int rows, int64_t out_row0, int out_ld, int out_col,
+                                          bf16_t* __restrict__ C, char* lds) {
+    const int lane = threadIdx.x & 63;
+    const int w = threadIdx.x >> 6;
+    f32x4_t acc[MT][SK_NF];
+#pragma unroll
+    for (int t = 0; t < MT; ++t)
+#pragma unroll
+        for (int f = 0; f < SK_NF; ++f) acc[t][f] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    if (s1 > s0) stream_mma<MT, 2>(wp, xp, s0, s1, acc);
+    f32x4_t* r4 = reinterpret_cast<f32x4_t*>(lds);  // [wave][t][f][lane]
+#pragma unroll
+    for (int t = 0; t < MT; ++t)
+#pragma unroll
+        for (int f = 0; f < SK_NF; ++f) r4[((w * MT + t) * SK_NF + f) * 64 + lane] = acc[t][f];
+    __syncthreads();
+    if (w != 0) return;  // no barrier follows
+#pragma unroll
+    for (int t = 0; t < MT; ++t)
+#pragma unroll
+        for (int f = 0; f < SK_NF; ++f) {
+            f32x4_t v = r4[(t * SK_NF + f) * 64 + lane];
+#pragma unroll
+            for (int ww = 1; ww < 4; ++ww) v += r4[((ww * MT + t) * SK_NF + f) * 64 + lane];
+            acc[t][f] = v;
+        }
+    stream_store<MODE, MT>(acc, rows, out_row0, out_ld, out_col, C, lane);
+}
+
+template <int MODE>
+__device__ __forceinline__ void tail_block(const bf16_t* __restrict__ A,
+                                           const int* __restrict__ row_token,
+                                           const bf16_t* __restrict__ B,
+                                           const int* __restrict__ offsets,
+                                           const int* __restrict__ tail_list, int task, int d,
+                                           int m, int tile_rows, bf16_t* __restrict__ C,
+                                           char* lds) {
+    const int per_e = (MODE == 0) ? m / 32 : d / 64;
+    const int i = task / per_e, c = task - i * per_e;
+    if (i >= tail_list[0]) return;  // block-uniform, before any barrier
+    const int e = tail_list[1 + i];
+    const int ce = offsets[e + 1] - offsets[e];
+    const int full = ce / tile_rows * tile_rows;
+    const int rows = ce - full;  // 1..kTailRows (32) by the plan
+    const int row0 = offsets[e] + full;
+    const int lane = threadIdx.x & 63;
+    const int w = threadIdx.x >> 6;
+    const int ns = ((MODE == 0) ? d : m) / 64;
+    const int s0 = ns * w / 4, s1 = ns * (w + 1) / 4;
+    const bf16_t* wp[SK_NF];
+    const bf16_t* xp[2];
+    stream_task<MODE, 2>(A, row_token, B, e, c, row0, rows, d, m, lane, wp, xp);
+    const int out_ld = (MODE == 0) ? m : d;
+    const int out_col = (MODE == 0) ? 32 * c : 64 * c;
+    if (rows <= 16) tail_task<MODE, 1>(wp, xp, s0, s1, rows, row0, out_ld, out_col, C, lds);
+    else tail_task<MODE, 2>(wp, xp, s0, s1, rows, row0, out_ld, out_col, C, lds);
+}
+
 template <int MODE>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) void gemm_bf16_dma(
     const bf16_t* __restrict__ A, const int* __restrict__ row_token,
     const bf16_t* __restrict__ B, const int* __restrict__ offsets,
-    const int* __restrict__ tile_off, int N, int d, int m, bf16_t* __restrict__ C) {
+    const int* __restrict__ tile_off, const int* __restrict__ tail_list, int big_blocks,
+    int N, int d, int m, bf16_t* __restrict__ C) {
     constexpr int TM = 256, TN = 256, TK = 64;
     constexpr int UNIT = TM * TK;  // elements of one ring unit: the A or the B half of a k-tile
     constexpr int NU = 5;          // units in the ring
@@ -270,6 +336,11 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
     // the compiler that all of it may be written there.
     __shared__ __attribute__((aligned(1024))) char sm_bytes[NU * UNIT * 2];
     bf16_t* const sm = reinterpret_cast<bf16_t*>(sm_bytes);
+    if ((int)blockIdx.x >= big_blocks) {  // the remainder blocks after the tiles
+        tail_block<MODE>(A, row_token, B, offsets, tail_list, (int)blockIdx.x - big_blocks, d,
+                         m, TM, C, sm_bytes);
+        return;
+    }
 
     const int nt_count = (MODE == 0) ? m / 128 : (d + TN - 1) / TN;
     int tile, ntile;
@@ -588,15 +659,17 @@ int gemm_tile_rows(int dtype, int64_t T, int K, int N, int d, int m) {
 }
 
 hipError_t launch_gemm_gate_up(const void* x, const void* Wgu, const int* row_token,
-                               const int* offsets, const int* tile_off, int64_t max_tiles,
-                               int tile_rows, int d, int N, int m, int dtype, void* H,
-                               hipStream_t s) {
+                               const int* offsets, const int* tile_off, const int* tail_list,
+                               int64_t max_tiles, int tile_rows, int d, int N, int m,
+                               int dtype, void* H, hipStream_t s) {
     if (max_tiles <= 0) return hipSuccess;
     if (dtype == ELB_BF16 && tile_rows == LBM) {
         ProfileScope prof("gemm_gate_up_bf16", s);
-        hipLaunchKernelGGL(gemm_bf16_dma<0>, dim3(grid8(max_tiles * (m / 128))),
-                           dim3(256), 0, s, (const bf16_t*)x, row_token, (const bf16_t*)Wgu,
-                           offsets, tile_off, N, d, m, (bf16_t*)H);
+        const unsigned big = grid8(max_tiles * (m / 128));
+        const unsigned tail = tail_list ? (unsigned)(kTailMax * (m / 32)) : 0u;
+        hipLaunchKernelGGL(gemm_bf16_dma<0>, dim3(big + tail), dim3(256), 0, s,
+                           (const bf16_t*)x, row_token, (const bf16_t*)Wgu, offsets, tile_off,
+                           tail_list, (int)big, N, d, m, (bf16_t*)H);
     } else if (dtype == ELB_BF16) {
         ProfileScope prof("gemm_gate_up_bf16_s", s);
         hipLaunchKernelGGL(gemm_bf16<0>, dim3(grid8(max_tiles * (m / 64))), dim3(256),
@@ -612,14 +685,17 @@ hipError_t launch_gemm_gate_up(const void* x, const void* Wgu, const int* row_to
 }
 
 hipError_t launch_gemm_down(const void* H, const void* Wd, const int* offsets,
-                            const int* tile_off, int64_t max_tiles, int tile_rows, int d, int N,
-                            int m, int dtype, void* Y, hipStream_t s) {
+                            const int* tile_off, const int* tail_list, int64_t max_tiles,
+                            int tile_rows, int d, int N, int m, int dtype, void* Y,
+                            hipStream_t s) {
     if (max_tiles <= 0) return hipSuccess;
     if (dtype == ELB_BF16 && tile_rows == LBM) {
         ProfileScope prof("gemm_down_bf16", s);
-        hipLaunchKernelGGL(gemm_bf16_dma<1>, dim3(grid8(max_tiles * ((d + LBN - 1) / LBN))),
-                           dim3(256), 0, s, (const bf16_t*)H, (const int*)nullptr,
-                           (const bf16_t*)Wd, offsets, tile_off, N, d, m, (bf16_t*)Y);
+        const unsigned big = grid8(max_tiles * ((d + LBN - 1) / LBN));
+        const unsigned tail = tail_list ? (unsigned)(kTailMax * (d / 64)) : 0u;
+        hipLaunchKernelGGL(gemm_bf16_dma<1>, dim3(big + tail), dim3(256), 0, s,
+                           (const bf16_t*)H, (const int*)nullptr, (const bf16_t*)Wd, offsets,
+                           tile_off, tail_list, (int)big, N, d, m, (bf16_t*)Y);
     } else if (dtype == ELB_BF16) {
         ProfileScope prof("gemm_down_bf16_s", s);
         hipLaunchKernelGGL(gemm_bf16<1>, dim3(grid8(max_tiles * ((d + BN - 1) / BN))),

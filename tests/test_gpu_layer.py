@@ -143,6 +143,31 @@ def test_experts_bf16_large_tiles_ragged(T, d, N, m, K):
     _experts_case(L, BF, K, O.MODE_TOPK, RTOL_BF16)
 
 
+@pytest.mark.parametrize("rems", [[1, 9, 17, 32] * 4, [5] * 15 + [0], [32] * 8 + [33] * 8])
+def test_experts_large_tiles_remainder_rows(rems):
+    """Experts of 256 + r rows on the 256-row tile path.  Remainders of at most 32 rows go to
+    the tail kernel when that saves a round of blocks (m = 2048: 16 tiles across per M-tile,
+    so 16 M-tiles per round on 256 compute units): the first two cases take it (32 -> 16 and
+    31 -> 16 M-tiles), the third does not (32 -> 24, still two rounds).  Every row is
+    compared with the oracle."""
+    N, d, m = 16, 128, 2048
+    counts = np.array([256 + r for r in rems])
+    T = int(counts.sum())
+    L = synth.moe_layer(T, d, N, m, dtype="bf16", seed=int(counts[0]) + len(rems))
+    rng = np.random.default_rng(int(counts.sum()))
+    ids = rng.permutation(np.repeat(np.arange(N), counts)).astype(np.int32)[:, None]
+    k = np.ones(T, np.int32)
+    w = rng.uniform(0.2, 1.0, (T, 1)).astype(np.float32)
+    x, _, Wgu, Wd = _layer_gpu(L, BF)
+    y = B.elb_moe_experts(x, Wgu, Wd, to_gpu(k, torch.int32), to_gpu(ids, torch.int32),
+                          to_gpu(w))
+    torch.cuda.synchronize()
+    ref = O.moe_experts(L.x, L.W_gu, L.W_down, k, ids, w.astype(np.float64))
+    rel = rel_err_rows(cpu(y), ref)
+    print("remainders %s: %d tokens, max rel %.3e" % (sorted(set(rems)), T, rel.max()))
+    assert rel.max() < RTOL_BF16
+
+
 @pytest.mark.parametrize("mode", [O.MODE_ELBOW, O.MODE_TOPK])
 def test_experts_bf16_olmoe_sampled(olmoe, mode):
     L = olmoe[0]
