@@ -120,3 +120,27 @@ def test_router_route_validation():
     assert call(d=100) == INVALID                          # bf16 router needs d % 32 == 0
     assert call(p=B.RouteParams(8, -1.0, 0, 0)) == INVALID
     assert call(T=0) == OK
+
+
+def test_variant_entry_points_validation():
+    lib = B.lib()
+    p = B.RouteParams(8, 1e-8, 0, 0)
+    tr = lambda T=10, N=64, p=p, rand=DUMMY, ptr=DUMMY: lib.elb_route_tail_random(
+        ptr, rand, T, N, C.byref(p) if p is not None else None, ptr, ptr, ptr, None)
+    assert tr(T=-1) == INVALID
+    assert tr(N=65) == UNSUPPORTED
+    assert tr(p=B.RouteParams(65, 1e-8, 0, 0)) == INVALID      # K > N
+    assert tr(p=None) == INVALID
+    assert tr(rand=None) == INVALID                             # the draws are required
+    assert tr(T=0, rand=None, ptr=None) == OK
+    ang = lambda T=10, N=64, eps=1e-8, lg=DUMMY, e=DUMMY, th=DUMMY: lib.elb_elbow_angle(
+        lg, T, N, eps, e, th, None)
+    assert ang(N=1) == INVALID
+    assert ang(N=65) == UNSUPPORTED
+    assert ang(eps=-1.0) == INVALID
+    assert ang(eps=float("inf")) == INVALID
+    assert ang(lg=None) == INVALID
+    assert ang(e=None, th=None) == OK                           # nothing asked for
+    assert ang(T=0, lg=None) == OK
+    # caps up to N are valid for the plain routing now (K = N: the uncapped elbow)
+    assert _route(10, 64, K=64, ptr=None) == INVALID            # only the NULL pointers fail
