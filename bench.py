@@ -45,14 +45,14 @@ def sha1(path):
     return hashlib.sha1(open(path, "rb").read()).hexdigest()[:12]
 
 
-def time_layer(B, torch, args_gpu, K, mode, steps, warmup, profile):
+def time_layer(B, torch, args_gpu, K, mode, steps, warmup, profile, packed=None):
     """Average ms per whole-layer call over `steps` calls (after `warmup`), and the average
     duration of each kernel from the library's per-launch hipEvents when `profile`."""
     x, Wr, Wgu, Wd = args_gpu
     out = torch.empty_like(x)
 
     def step():
-        B.elb_moe_forward(x, Wr, Wgu, Wd, K=K, mode=mode, out=out)
+        B.elb_moe_forward(x, Wr, Wgu, Wd, K=K, mode=mode, out=out, packed=packed)
     for _ in range(warmup):
         step()
     torch.cuda.synchronize()
@@ -162,21 +162,28 @@ def routing_variants(B, torch, T=65536, N=64, K=8, nbuf=16, iters=48):
 
 def decode_layer(B, torch, synth, K=8, steps=100):
     """The OLMoE-shaped layer at a decode batch (T = 64): latency per layer call, elbow and
-    top-8, and the weight stream of the expert GEMMs against HBM bandwidth."""
+    top-8, with the expert weights in their packed copy (elb_pack_expert_weights, made once
+    before timing) and, for comparison, row-major; and the weight stream of the expert GEMMs
+    against HBM bandwidth (packed)."""
     T, d, N, m = WORKLOADS["olmoe-decode"][:4]
     L = synth.moe_layer(T, d, N, m, dtype="bf16", seed=0)
     gpu = tuple(torch.from_numpy(a).to("cuda").to(torch.bfloat16)
                 for a in (L.x, L.W_router, L.W_gu, L.W_down))
-    _, dbg = B.elb_moe_forward(*gpu, K=K, debug=True)
+    packed = B.elb_pack_expert_weights(gpu[2], gpu[3])
+    _, dbg = B.elb_moe_forward(*gpu, K=K, debug=True, packed=packed)
     torch.cuda.synchronize()
     counts = dbg["counts"].cpu().numpy()
     sum_k, used = int(counts.sum()), int((counts > 0).sum())
-    out = {"workload": "olmoe-decode: T=%d d_model=%d N=%d m=%d K=%d bf16" % (T, d, N, m, K),
+    out = {"workload": "olmoe-decode: T=%d d_model=%d N=%d m=%d K=%d bf16, packed expert "
+                       "weights" % (T, d, N, m, K),
            "experts_used": used, "mean_k": round(sum_k / T, 4)}
     for name, mode in (("elbow", B.MODE_ELBOW), ("topk", B.MODE_TOPK)):
-        ms, _ = time_layer(B, torch, gpu, K, mode, steps, 10, False)
+        ms, _ = time_layer(B, torch, gpu, K, mode, steps, 10, False, packed)
         out[name] = {"us_per_layer": round(ms * 1e3, 2), "tokens_per_s": round(T / ms * 1e3, 1)}
-    _, kern = time_layer(B, torch, gpu, K, B.MODE_ELBOW, steps, 2, True)
+    ms, _ = time_layer(B, torch, gpu, K, B.MODE_ELBOW, steps, 10, False)
+    out["elbow_row_major_weights"] = {"us_per_layer": round(ms * 1e3, 2),
+                                      "tokens_per_s": round(T / ms * 1e3, 1)}
+    _, kern = time_layer(B, torch, gpu, K, B.MODE_ELBOW, steps, 2, True, packed)
     out["kernels_us"] = {n: round(v * 1e3, 2) for n, v in kern.items()}
     g1 = next(n for n in kern if n.startswith("gemm_gate_up"))
     g2 = next(n for n in kern if n.startswith("gemm_down"))

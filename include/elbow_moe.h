@@ -209,6 +209,37 @@ int elb_moe_forward(const void *x, const void *W_router, const void *W_gate_up,
                     void *stream);
 
 /*
+ * Packed expert weights for decode-sized batches.  When an expert gets at most 16 rows on
+ * average (T K <= 16 N), the expert GEMMs are bound by reading the weights; the layer then
+ * streams each expert's weights in 64-row tasks.  elb_pack_expert_weights writes a copy of
+ * W_gate_up and W_down in exactly that streaming order (per task, stage and MFMA operand, the
+ * 64 lanes' 16-byte pieces contiguous), so that every load reads 1 KB contiguous; it is done
+ * once, outside the per-call path.  The packed copy has the size of the two weight tensors
+ * together (elb_packed_expert_bytes), is bf16 only (d % 64 == 0, m % 64 == 0) and is valid
+ * until the weights change.
+ *   W_gate_up [N, 2m, d], W_down [N, d, m]   bf16 input (as for elb_moe_experts)
+ *   packed                                   device output, elb_packed_expert_bytes bytes
+ * elb_moe_experts_packed / elb_moe_forward_packed are elb_moe_experts / elb_moe_forward with
+ * that copy as an extra argument: the decode-sized kernels read it, every other path reads
+ * W_gate_up and W_down as usual (so both are still required).  Results are bit-identical to
+ * the unpacked calls.
+ */
+size_t elb_packed_expert_bytes(int32_t N, int32_t d, int32_t m);
+int elb_pack_expert_weights(const void *W_gate_up, const void *W_down, int32_t N, int32_t d,
+                            int32_t m, int32_t dtype, void *packed, void *stream);
+int elb_moe_experts_packed(const void *x, const void *W_gate_up, const void *W_down,
+                           const void *packed, const int32_t *k, const int32_t *ids,
+                           const float *w, const void *residual, int64_t T, int32_t d,
+                           int32_t N, int32_t m, int32_t K, int32_t dtype, void *y,
+                           void *workspace, size_t workspace_bytes, void *stream);
+int elb_moe_forward_packed(const void *x, const void *W_router, const void *W_gate_up,
+                           const void *W_down, const void *packed, const void *residual,
+                           int64_t T, int32_t d, int32_t N, int32_t m, int32_t dtype,
+                           const elb_route_params *params, void *y, void *workspace,
+                           size_t workspace_bytes, float *logits_out, int32_t *k_out,
+                           int32_t *ids_out, float *w_out, int32_t *counts_out, void *stream);
+
+/*
  * Per-kernel timing (host-side hipEvents around each launch the library makes).
  * elb_profile_enable(1) starts recording on the calling process; every launch then
  * records a start/stop event pair on its stream.  elb_profile_read() synchronises on the

@@ -62,6 +62,13 @@ def lib():
                             C.c_int),
         "elb_moe_forward": ([P, P, P, P, P, I64, I32, I32, I32, I32, C.POINTER(RouteParams), P,
                              P, SZ, P, P, P, P, P, P], C.c_int),
+        "elb_packed_expert_bytes": ([I32, I32, I32], SZ),
+        "elb_pack_expert_weights": ([P, P, I32, I32, I32, I32, P, P], C.c_int),
+        "elb_moe_experts_packed": ([P, P, P, P, P, P, P, P, I64, I32, I32, I32, I32, I32, P, P,
+                                    SZ, P], C.c_int),
+        "elb_moe_forward_packed": ([P, P, P, P, P, P, I64, I32, I32, I32, I32,
+                                    C.POINTER(RouteParams), P, P, SZ, P, P, P, P, P, P],
+                                   C.c_int),
         "elb_profile_enable": ([C.c_int], C.c_int),
         "elb_profile_read": ([C.POINTER(C.c_char_p), C.POINTER(C.c_double),
                               C.POINTER(C.c_int64), C.c_int], C.c_int),
@@ -223,8 +230,23 @@ def elb_moe_workspace_bytes(T: int, d: int, N: int, m: int, K: int, dtype: int) 
     return int(lib().elb_moe_workspace_bytes(T, d, N, m, K, dtype))
 
 
-def elb_moe_experts(x, W_gate_up, W_down, k, ids, w, residual=None, out=None) -> torch.Tensor:
-    _dev(x, W_gate_up, W_down, k, ids, w, residual, out)
+def elb_pack_expert_weights(W_gate_up: torch.Tensor, W_down: torch.Tensor) -> torch.Tensor:
+    """The packed copy of bf16 expert weights for the decode-sized path (uint8 tensor)."""
+    _dev(W_gate_up, W_down)
+    N, m2, d = W_gate_up.shape
+    m = m2 // 2
+    packed = torch.empty(int(lib().elb_packed_expert_bytes(N, d, m)), dtype=torch.uint8,
+                         device=W_gate_up.device)
+    _check("elb_pack_expert_weights", lib().elb_pack_expert_weights(
+        _ptr(W_gate_up), _ptr(W_down), N, d, m, _dtype_code(W_gate_up), _ptr(packed),
+        _stream()))
+    return packed
+
+
+def elb_moe_experts(x, W_gate_up, W_down, k, ids, w, residual=None, out=None,
+                    packed=None) -> torch.Tensor:
+    """packed: optional packed weights (elb_pack_expert_weights) for the decode-sized path."""
+    _dev(x, W_gate_up, W_down, k, ids, w, residual, out, packed)
     T, d = x.shape
     N, m2, _ = W_gate_up.shape
     m = m2 // 2
@@ -233,17 +255,23 @@ def elb_moe_experts(x, W_gate_up, W_down, k, ids, w, residual=None, out=None) ->
     y = torch.empty_like(x) if out is None else out
     nb = elb_moe_workspace_bytes(T, d, N, m, K, dt)
     ws = workspace(nb, x.device)
-    _check("elb_moe_experts", lib().elb_moe_experts(
-        _ptr(x), _ptr(W_gate_up), _ptr(W_down), _ptr(k), _ptr(ids), _ptr(w), _ptr(residual),
-        T, d, N, m, K, dt, _ptr(y), _ptr(ws), ws.numel(), _stream()))
+    if packed is None:
+        _check("elb_moe_experts", lib().elb_moe_experts(
+            _ptr(x), _ptr(W_gate_up), _ptr(W_down), _ptr(k), _ptr(ids), _ptr(w),
+            _ptr(residual), T, d, N, m, K, dt, _ptr(y), _ptr(ws), ws.numel(), _stream()))
+    else:
+        _check("elb_moe_experts_packed", lib().elb_moe_experts_packed(
+            _ptr(x), _ptr(W_gate_up), _ptr(W_down), _ptr(packed), _ptr(k), _ptr(ids), _ptr(w),
+            _ptr(residual), T, d, N, m, K, dt, _ptr(y), _ptr(ws), ws.numel(), _stream()))
     return y
 
 
 def elb_moe_forward(x, W_router, W_gate_up, W_down, K: int = 8, eps: float = 1e-8,
                     mode: int = MODE_ELBOW, renormalize: bool = False, residual=None,
-                    out=None, debug: bool = False):
-    """The whole layer.  Returns y, or (y, dict of intermediates) when debug=True."""
-    _dev(x, W_router, W_gate_up, W_down, residual, out)
+                    out=None, debug: bool = False, packed=None):
+    """The whole layer.  Returns y, or (y, dict of intermediates) when debug=True.
+    packed: optional packed weights (elb_pack_expert_weights) for the decode-sized path."""
+    _dev(x, W_router, W_gate_up, W_down, residual, out, packed)
     T, d = x.shape
     N = W_router.shape[0]
     m = W_down.shape[2]
@@ -260,11 +288,16 @@ def elb_moe_forward(x, W_router, W_gate_up, W_down, K: int = 8, eps: float = 1e-
                "w": torch.empty((T, K), dtype=torch.float32, device=dev),
                "counts": torch.empty(N, dtype=torch.int32, device=dev)}
     p = RouteParams(K, eps, mode, int(renormalize))
-    _check("elb_moe_forward", lib().elb_moe_forward(
-        _ptr(x), _ptr(W_router), _ptr(W_gate_up), _ptr(W_down), _ptr(residual), T, d, N, m,
-        dt, C.byref(p), _ptr(y), _ptr(ws), ws.numel(), _ptr(dbg.get("logits")),
-        _ptr(dbg.get("k")), _ptr(dbg.get("ids")), _ptr(dbg.get("w")), _ptr(dbg.get("counts")),
-        _stream()))
+    tail = (_ptr(dbg.get("logits")), _ptr(dbg.get("k")), _ptr(dbg.get("ids")),
+            _ptr(dbg.get("w")), _ptr(dbg.get("counts")), _stream())
+    if packed is None:
+        _check("elb_moe_forward", lib().elb_moe_forward(
+            _ptr(x), _ptr(W_router), _ptr(W_gate_up), _ptr(W_down), _ptr(residual), T, d, N, m,
+            dt, C.byref(p), _ptr(y), _ptr(ws), ws.numel(), *tail))
+    else:
+        _check("elb_moe_forward_packed", lib().elb_moe_forward_packed(
+            _ptr(x), _ptr(W_router), _ptr(W_gate_up), _ptr(W_down), _ptr(packed),
+            _ptr(residual), T, d, N, m, dt, C.byref(p), _ptr(y), _ptr(ws), ws.numel(), *tail))
     return (y, dbg) if debug else y
 
 

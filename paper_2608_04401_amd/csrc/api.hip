@@ -306,6 +306,7 @@ size_t elb_moe_workspace_bytes(int64_t T, int32_t d, int32_t N, int32_t m, int32
 }
 
 static int experts_impl(const void* x, const void* W_gate_up, const void* W_down,
+                        const void* packed,
                         const int32_t* k, const int32_t* ids, const float* w,
                         const void* residual, int64_t T, int d, int N, int m, int K, int dtype,
                         void* y, char* ws, const Layout& L, int32_t* counts_out,
@@ -330,7 +331,7 @@ static int experts_impl(const void* x, const void* W_gate_up, const void* W_down
                                             hist, tile_off, tail_list, plan, s), "dispatch"))
         return rc;
     if (gemm_use_skinny(dtype, T, K, N, d, m)) {
-        if (int rc = hip_status(launch_gemm_skinny(x, W_gate_up, W_down, row_token, offsets, d,
+        if (int rc = hip_status(launch_gemm_skinny(x, W_gate_up, W_down, packed, row_token, offsets, d,
                                                    N, m, H, Y, s), "gemm_skinny"))
             return rc;
     } else {
@@ -348,7 +349,8 @@ static int experts_impl(const void* x, const void* W_gate_up, const void* W_down
     return hip_status(launch_combine(Y, k, inv, w, residual, T, d, K, dtype, y, s), "combine");
 }
 
-int elb_moe_experts(const void* x, const void* W_gate_up, const void* W_down,
+static int moe_experts_entry(const void* x, const void* W_gate_up, const void* W_down,
+                             const void* packed,
                     const int32_t* k, const int32_t* ids, const float* w, const void* residual,
                     int64_t T, int32_t d, int32_t N, int32_t m, int32_t K, int32_t dtype,
                     void* y, void* workspace, size_t workspace_bytes, void* stream) {
@@ -361,12 +363,29 @@ int elb_moe_experts(const void* x, const void* W_gate_up, const void* W_down,
     if (!workspace || workspace_bytes < L.experts_end)
         return fail(ELB_ERR_WORKSPACE, "workspace of %zu bytes, need %zu", workspace_bytes,
                     L.experts_end);
-    return experts_impl(x, W_gate_up, W_down, k, ids, w, residual, T, d, N, m, K, dtype, y,
+    return experts_impl(x, W_gate_up, W_down, packed, k, ids, w, residual, T, d, N, m, K, dtype, y,
                         (char*)workspace, L, nullptr, (hipStream_t)stream);
 }
 
-int elb_moe_forward(const void* x, const void* W_router, const void* W_gate_up,
-                    const void* W_down, const void* residual, int64_t T, int32_t d, int32_t N,
+int elb_moe_experts(const void* x, const void* W_gate_up, const void* W_down,
+                    const int32_t* k, const int32_t* ids, const float* w, const void* residual,
+                    int64_t T, int32_t d, int32_t N, int32_t m, int32_t K, int32_t dtype,
+                    void* y, void* workspace, size_t workspace_bytes, void* stream) {
+    return moe_experts_entry(x, W_gate_up, W_down, nullptr, k, ids, w, residual, T, d, N, m, K,
+                             dtype, y, workspace, workspace_bytes, stream);
+}
+
+int elb_moe_experts_packed(const void* x, const void* W_gate_up, const void* W_down,
+                           const void* packed, const int32_t* k, const int32_t* ids,
+                           const float* w, const void* residual, int64_t T, int32_t d,
+                           int32_t N, int32_t m, int32_t K, int32_t dtype, void* y,
+                           void* workspace, size_t workspace_bytes, void* stream) {
+    return moe_experts_entry(x, W_gate_up, W_down, packed, k, ids, w, residual, T, d, N, m, K,
+                             dtype, y, workspace, workspace_bytes, stream);
+}
+
+static int moe_forward_entry(const void* x, const void* W_router, const void* W_gate_up,
+                             const void* W_down, const void* packed, const void* residual, int64_t T, int32_t d, int32_t N,
                     int32_t m, int32_t dtype, const elb_route_params* params, void* y,
                     void* workspace, size_t workspace_bytes, float* logits_out,
                     int32_t* k_out, int32_t* ids_out, float* w_out, int32_t* counts_out,
@@ -399,8 +418,51 @@ int elb_moe_forward(const void* x, const void* W_router, const void* W_gate_up,
         if (int rc = hip_status(launch_route(logits, T, N, *params, k, ids, w, s), "route"))
             return rc;
     }
-    return experts_impl(x, W_gate_up, W_down, k, ids, w, residual, T, d, N, m, K, dtype, y, ws,
+    return experts_impl(x, W_gate_up, W_down, packed, k, ids, w, residual, T, d, N, m, K, dtype, y, ws,
                         L, counts_out, s);
+}
+
+int elb_moe_forward(const void* x, const void* W_router, const void* W_gate_up,
+                    const void* W_down, const void* residual, int64_t T, int32_t d, int32_t N,
+                    int32_t m, int32_t dtype, const elb_route_params* params, void* y,
+                    void* workspace, size_t workspace_bytes, float* logits_out,
+                    int32_t* k_out, int32_t* ids_out, float* w_out, int32_t* counts_out,
+                    void* stream) {
+    return moe_forward_entry(x, W_router, W_gate_up, W_down, nullptr, residual, T, d, N, m,
+                             dtype, params, y, workspace, workspace_bytes, logits_out, k_out,
+                             ids_out, w_out, counts_out, stream);
+}
+
+int elb_moe_forward_packed(const void* x, const void* W_router, const void* W_gate_up,
+                           const void* W_down, const void* packed, const void* residual,
+                           int64_t T, int32_t d, int32_t N, int32_t m, int32_t dtype,
+                           const elb_route_params* params, void* y, void* workspace,
+                           size_t workspace_bytes, float* logits_out, int32_t* k_out,
+                           int32_t* ids_out, float* w_out, int32_t* counts_out, void* stream) {
+    return moe_forward_entry(x, W_router, W_gate_up, W_down, packed, residual, T, d, N, m,
+                             dtype, params, y, workspace, workspace_bytes, logits_out, k_out,
+                             ids_out, w_out, counts_out, stream);
+}
+
+size_t elb_packed_expert_bytes(int32_t N, int32_t d, int32_t m) {
+    if (N < 1 || d < 1 || m < 1) return 0;
+    return ((size_t)N * 2 * m * d + (size_t)N * d * m) * 2;
+}
+
+int elb_pack_expert_weights(const void* W_gate_up, const void* W_down, int32_t N, int32_t d,
+                            int32_t m, int32_t dtype, void* packed, void* stream) {
+    g_err.clear();
+    if (dtype != ELB_BF16)
+        return fail(ELB_ERR_UNSUPPORTED, "packed expert weights are bf16 only");
+    if (N < 1 || N > ELB_MAX_EXPERTS)
+        return fail(ELB_ERR_INVALID_ARG, "N = %d outside [1, %d]", N, ELB_MAX_EXPERTS);
+    if (d < 64 || m < 64 || d % 64 || m % 64)
+        return fail(ELB_ERR_INVALID_ARG, "d = %d and m = %d must be positive multiples of 64",
+                    d, m);
+    if (!W_gate_up || !W_down || !packed) return fail(ELB_ERR_INVALID_ARG, "NULL tensor pointer");
+    return hip_status(launch_pack_experts(W_gate_up, W_down, N, d, m, packed,
+                                          (hipStream_t)stream),
+                      "pack_experts");
 }
 
 int elb_profile_enable(int on) {

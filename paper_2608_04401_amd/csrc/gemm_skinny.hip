@@ -32,7 +32,7 @@ namespace {
 constexpr int SK_MAXMT = 2;  // token tiles of 16 rows per chunk (32 rows)
 
 // One chunk of up to 16 * MT token rows of a task over the whole contraction.
-template <int MODE, int MT>
+template <int MODE, int MT, bool PACKED>
 __device__ __forceinline__ void skinny_chunk(const bf16_t* const (&wp)[SK_NF],
                                              const bf16_t* const (&xp)[SK_MAXMT], int kd,
                                              int rows, int64_t out_row0, int out_ld,
@@ -42,13 +42,14 @@ __device__ __forceinline__ void skinny_chunk(const bf16_t* const (&wp)[SK_NF],
     for (int t = 0; t < MT; ++t)
 #pragma unroll
         for (int f = 0; f < SK_NF; ++f) acc[t][f] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-    stream_mma<MT, SK_MAXMT>(wp, xp, 0, kd / 64, acc);
+    stream_mma<MT, SK_MAXMT, 3, PACKED>(wp, xp, 0, kd / 64, acc);
     stream_store<MODE, MT>(acc, rows, out_row0, out_ld, out_col, C, lane);
 }
 
 // MODE 0: A = x [T, d] gathered through row_token, W = W_gate_up [N, 2m, d], C = H [rows, m]
 // MODE 1: A = H [rows, m], W = W_down [N, d, m], C = Y [rows, d]
-template <int MODE>
+// PACKED: W is the packed copy of those weights (elb_pack_expert_weights)
+template <int MODE, bool PACKED>
 // (2 waves per SIMD: the register ring of three stages fits in 256 registers)
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) void gemm_skinny(
     const bf16_t* __restrict__ A, const int* __restrict__ row_token,
@@ -76,10 +77,49 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
         const bf16_t* wp[SK_NF];
         const bf16_t* xp[SK_MAXMT];
         stream_task<MODE, SK_MAXMT>(A, row_token, W, e, c, row0 + cb, rows, d, m, lane, wp, xp);
+        if (PACKED) stream_task_packed<MODE>(W, e, c, d, m, lane, wp);
         const int64_t orow = row0 + cb;
-        if (rows <= 16) skinny_chunk<MODE, 1>(wp, xp, kd, rows, orow, out_ld, out_col, C, lane);
-        else skinny_chunk<MODE, 2>(wp, xp, kd, rows, orow, out_ld, out_col, C, lane);
+        if (rows <= 16)
+            skinny_chunk<MODE, 1, PACKED>(wp, xp, kd, rows, orow, out_ld, out_col, C, lane);
+        else
+            skinny_chunk<MODE, 2, PACKED>(wp, xp, kd, rows, orow, out_ld, out_col, C, lane);
     }
+}
+
+// Packing: one thread per 16-byte operand of the packed copy, in packed order, gathered from
+// the row-major weights (gate/up then down; the packed copy has the same size).
+__global__ __launch_bounds__(256) void pack_experts(const bf16_t* __restrict__ Wgu,
+                                                    const bf16_t* __restrict__ Wd, int N, int d,
+                                                    int m, bf16_t* __restrict__ P) {
+    const int64_t n_gu = (int64_t)N * 2 * m * d / 8;  // 16-byte operands of W_gate_up
+    const int64_t n_all = n_gu + (int64_t)N * d * m / 8;
+    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (i >= n_all) return;
+    const bool gu = i < n_gu;
+    const int64_t j = gu ? i : i - n_gu;
+    const int lane = (int)(j % 64);
+    int64_t q = j / 64;
+    const int f = (int)(q % 4);
+    q /= 4;
+    const int h = (int)(q % 2);
+    q /= 2;
+    const int ns = (gu ? d : m) / 64;
+    const int s = (int)(q % ns);
+    q /= ns;
+    const int per_e = gu ? m / 32 : d / 64;
+    const int c = (int)(q % per_e);
+    const int e = (int)(q / per_e);
+    const int l16 = lane & 15, kq = (lane >> 4) * 8;
+    const int k = 64 * s + 32 * h + kq;
+    int64_t src;
+    if (gu) {
+        const int wrow = (f < 2) ? 32 * c + 16 * f + l16 : m + 32 * c + 16 * (f - 2) + l16;
+        src = ((int64_t)e * 2 * m + wrow) * d + k;
+    } else {
+        src = ((int64_t)e * d + 64 * c + 16 * f + l16) * m + k;
+    }
+    const u32x4_t v = *reinterpret_cast<const u32x4_t*>((gu ? Wgu : Wd) + src);
+    *reinterpret_cast<u32x4_t*>(P + i * 8) = v;
 }
 
 unsigned blocks_for(int tasks) { return (unsigned)(((tasks + 3) / 4 + 7) / 8 * 8); }
@@ -93,22 +133,44 @@ bool gemm_use_skinny(int dtype, int64_t T, int K, int N, int d, int m) {
            d % 64 == 0 && m % 64 == 0;
 }
 
-hipError_t launch_gemm_skinny(const void* x, const void* Wgu, const void* Wd,
+hipError_t launch_gemm_skinny(const void* x, const void* Wgu, const void* Wd, const void* packed,
                               const int* row_token, const int* offsets, int d, int N, int m,
                               void* H, void* Y, hipStream_t s) {
+    const bf16_t* pgu = (const bf16_t*)packed;
+    const bf16_t* pd = pgu ? pgu + (int64_t)N * 2 * m * d : nullptr;
     {
         ProfileScope prof("gemm_gate_up_skinny", s);
-        hipLaunchKernelGGL(gemm_skinny<0>, dim3(blocks_for(N * (m / 32))), dim3(256), 0, s,
-                           (const bf16_t*)x, row_token, (const bf16_t*)Wgu, offsets, N, d, m,
-                           (bf16_t*)H);
+        if (pgu)
+            hipLaunchKernelGGL((gemm_skinny<0, true>), dim3(blocks_for(N * (m / 32))), dim3(256),
+                               0, s, (const bf16_t*)x, row_token, pgu, offsets, N, d, m,
+                               (bf16_t*)H);
+        else
+            hipLaunchKernelGGL((gemm_skinny<0, false>), dim3(blocks_for(N * (m / 32))),
+                               dim3(256), 0, s, (const bf16_t*)x, row_token,
+                               (const bf16_t*)Wgu, offsets, N, d, m, (bf16_t*)H);
     }
     if (hipError_t e = hipGetLastError(); e != hipSuccess) return e;
     {
         ProfileScope prof("gemm_down_skinny", s);
-        hipLaunchKernelGGL(gemm_skinny<1>, dim3(blocks_for(N * (d / 64))), dim3(256), 0, s,
-                           (const bf16_t*)H, (const int*)nullptr, (const bf16_t*)Wd, offsets,
-                           N, d, m, (bf16_t*)Y);
+        if (pd)
+            hipLaunchKernelGGL((gemm_skinny<1, true>), dim3(blocks_for(N * (d / 64))), dim3(256),
+                               0, s, (const bf16_t*)H, (const int*)nullptr, pd, offsets, N, d,
+                               m, (bf16_t*)Y);
+        else
+            hipLaunchKernelGGL((gemm_skinny<1, false>), dim3(blocks_for(N * (d / 64))),
+                               dim3(256), 0, s, (const bf16_t*)H, (const int*)nullptr,
+                               (const bf16_t*)Wd, offsets, N, d, m, (bf16_t*)Y);
     }
+    return hipGetLastError();
+}
+
+hipError_t launch_pack_experts(const void* Wgu, const void* Wd, int N, int d, int m,
+                               void* packed, hipStream_t s) {
+    const int64_t n_all = ((int64_t)N * 2 * m * d + (int64_t)N * d * m) / 8;
+    if (n_all == 0) return hipSuccess;
+    ProfileScope prof("pack_experts", s);
+    hipLaunchKernelGGL(pack_experts, dim3((unsigned)((n_all + 255) / 256)), dim3(256), 0, s,
+                       (const bf16_t*)Wgu, (const bf16_t*)Wd, N, d, m, (bf16_t*)packed);
     return hipGetLastError();
 }
 

@@ -57,23 +57,49 @@ __device__ __forceinline__ void stream_task(const bf16_t* __restrict__ A,
     }
 }
 
+// Packed weights (elb_pack_expert_weights): a task's 64 weight rows are stored in the order
+// they are loaded -- per stage s, half h and fragment f, the 64 lanes' 16-byte operands
+// (weight row 16 f + lane % 16 of the task, k = 64 s + 32 h + 8 (lane / 16) .. + 8) -- so every
+// load instruction reads 1 KB contiguous and a task is one contiguous stream.
+constexpr int kPackUnit = 512;  // bf16 elements of one (stage, half, fragment) operand block
+
+// Lane addresses in a packed task (stage 0, half 0): wp[f] = task base + f units + lane's 16 B
+template <int MODE>
+__device__ __forceinline__ void stream_task_packed(const bf16_t* __restrict__ P, int e, int c,
+                                                   int d, int m, int lane,
+                                                   const bf16_t* (&wp)[SK_NF]) {
+    const int per_e = (MODE == 0) ? m / 32 : d / 64;
+    const int ns = ((MODE == 0) ? d : m) / 64;
+    const bf16_t* base = P + ((int64_t)e * per_e + c) * ns * (8 * kPackUnit);
+#pragma unroll
+    for (int f = 0; f < SK_NF; ++f) wp[f] = base + f * kPackUnit + lane * 8;
+}
+
 // acc[t][f] += the task's stages [s0, s1) (a stage is 64 of the contraction, two 32-deep
 // halves).  A ring of R register slots keeps R - 1 stages in flight: stage j lives in slot
 // j % R, and while stage j is multiplied, stage j + R - 1 is loaded into the slot stage j - 1
 // has just freed.  Unrolled by R, so every slot index is a constant.  Loads past the last
-// stage re-read it (clamped) and are never used.
-template <int MT, int MAXMT, int R = 3>
+// stage re-read it (clamped) and are never used.  PACKED: weights in the packed order, read
+// with the non-temporal hint (a contiguous stream read once).
+template <int MT, int MAXMT, int R = 3, bool PACKED = false>
 __device__ __forceinline__ void stream_mma(const bf16_t* const (&wp)[SK_NF],
                                            const bf16_t* const (&xp)[MAXMT], int s0, int s1,
                                            f32x4_t (&acc)[MT][SK_NF]) {
     bf16x8_t w[R][SK_NF][2], x[R][MT][2];
     auto load = [&](int j, bf16x8_t (&ws)[SK_NF][2], bf16x8_t (&xs)[MT][2]) {
-        const int k0 = (s0 + j < s1 ? s0 + j : s1 - 1) * 64;
+        const int s = s0 + j < s1 ? s0 + j : s1 - 1;
+        const int k0 = s * 64;
 #pragma unroll
         for (int h = 0; h < 2; ++h) {
 #pragma unroll
-            for (int f = 0; f < SK_NF; ++f)
-                ws[f][h] = *reinterpret_cast<const bf16x8_t*>(wp[f] + k0 + 32 * h);
+            for (int f = 0; f < SK_NF; ++f) {
+                if (PACKED)
+                    ws[f][h] = __builtin_bit_cast(
+                        bf16x8_t, __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(
+                                      wp[f] + (s * 8 + h * 4) * kPackUnit)));
+                else
+                    ws[f][h] = *reinterpret_cast<const bf16x8_t*>(wp[f] + k0 + 32 * h);
+            }
 #pragma unroll
             for (int t = 0; t < MT; ++t)
                 xs[t][h] = *reinterpret_cast<const bf16x8_t*>(xp[t] + k0 + 32 * h);

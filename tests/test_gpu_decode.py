@@ -74,3 +74,36 @@ def test_experts_decode_shapes(T, d, N, m, K):
     rel = _experts(L, r.k, r.ids, r.w.astype(np.float32))
     print("shape T=%d d=%d N=%d m=%d K=%d: max rel %.3e" % (T, d, N, m, K, rel.max()))
     assert rel.max() < RTOL_BF16
+
+
+@pytest.mark.parametrize("T", [1, 64, 128])
+def test_forward_decode_packed_weights_bit_identical(T):
+    """The packed copy of the weights gives the same bits as the row-major weights (same
+    operands, same accumulation order), and parity with the oracle."""
+    L = synth.olmoe_layer(T=T, seed=50 + T)
+    x, Wr, Wgu, Wd = _gpu(L)
+    packed = B.elb_pack_expert_weights(Wgu, Wd)
+    assert packed.numel() == (Wgu.numel() + Wd.numel()) * 2
+    y0 = B.elb_moe_forward(x, Wr, Wgu, Wd, K=8)
+    y1, dbg = B.elb_moe_forward(x, Wr, Wgu, Wd, K=8, packed=packed, debug=True)
+    torch.cuda.synchronize()
+    assert torch.equal(y0.view(torch.int16), y1.view(torch.int16))
+    ref = O.moe_forward(L.x, L.W_router, L.W_gu, L.W_down, K=8)
+    k, ids = cpu(dbg["k"]), cpu(dbg["ids"])
+    same = (k == ref.routing.k) & (ids == ref.routing.ids).all(axis=1)
+    assert (ref.routing.margin[~same] < NEAR_TIE).all()
+    assert rel_err_rows(cpu(y1)[same], ref.y[same]).max() < RTOL_BF16
+
+
+@pytest.mark.parametrize("T,d,N,m,K", [(7, 64, 8, 64, 3), (33, 320, 16, 192, 4)])
+def test_experts_decode_packed_small_widths(T, d, N, m, K):
+    L = synth.moe_layer(T, d, N, m, dtype="bf16", seed=T + d + 1)
+    r = O.route(O.router_logits(L.x, L.W_router).astype(np.float32), K=K)
+    x, _, Wgu, Wd = _gpu(L)
+    packed = B.elb_pack_expert_weights(Wgu, Wd)
+    args = (to_gpu(r.k, torch.int32), to_gpu(r.ids, torch.int32),
+            to_gpu(r.w.astype(np.float32)))
+    y0 = B.elb_moe_experts(x, Wgu, Wd, *args)
+    y1 = B.elb_moe_experts(x, Wgu, Wd, *args, packed=packed)
+    torch.cuda.synchronize()
+    assert torch.equal(y0.view(torch.int16), y1.view(torch.int16))
