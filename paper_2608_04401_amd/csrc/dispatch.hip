@@ -171,7 +171,7 @@ __global__ __launch_bounds__(256) void dispatch_scatter(const int* __restrict__ 
     for (int e = 0; e < N; ++e) {
         const bool has = (mask >> e) & 1ull;
         const uint64_t b = __ballot(has);
-        const int base = __shfl(base_mine, e);
+        const int base = __builtin_amdgcn_readlane(base_mine, e);  // e is wave-uniform
         if (has) {
             const int r = base + __popcll(b & below);
             row_token[r] = (int)t;
@@ -256,7 +256,7 @@ __global__ __launch_bounds__(256) void dispatch_small(const int* __restrict__ k,
     for (int e = 0; e < N; ++e) {
         const bool has = (mask >> e) & 1ull;
         const uint64_t b = __ballot(has);
-        const int bse = __shfl(base_mine, e);
+        const int bse = __builtin_amdgcn_readlane(base_mine, e);  // e is wave-uniform
         if (has) {
             const int r = bse + __popcll(b & below);
             row_token[r] = t;
