@@ -152,6 +152,11 @@ def routing_variants(B, torch, T=65536, N=64, K=8, nbuf=16, iters=48):
         "elbow_angle": (lambda i: B.elb_elbow_angle(bl[i % nbuf]), 4 * T * N + 8 * T),
     }
     out = {"workload": "routing-only T=%d N=%d planted logits, uniform draws" % (T, N)}
+    # the paper's elbow-angle statistic on this workload: share of tokens at or below 135 deg
+    e, theta = B.elb_elbow_angle(bl[0])
+    torch.cuda.synchronize()
+    out["angle_le_135_fraction"] = round(float((theta <= 135.0).float().mean().item()), 4)
+    out["angle_mean_deg"] = round(float(theta.mean().item()), 3)
     for name, (fn, nbytes) in cases.items():
         us = _profiled(B, torch, fn, iters)["route_pair"]
         gbs = nbytes / (us * 1e-6) / 1e9

@@ -327,14 +327,20 @@ static int experts_impl(const void* x, const void* W_gate_up, const void* W_down
     const bool big = (dtype == ELB_BF16 && tr == 256);
     const TilePlan plan{tr, big ? kTailRows : 0, big ? cus_per_device() / (m / 128) : 1,
                         kTailMax};
+    if (gemm_use_skinny(dtype, T, K, N, d, m)) {
+        // decode-sized: no dispatch; the expert waves find their slots from (k, ids) and
+        // write rows t K + j of H and Y, which the combine reads directly
+        if (int rc = hip_status(launch_gemm_skinny(x, W_gate_up, W_down, packed, k, ids, T, K,
+                                                   d, N, m, H, Y, counts_out, s),
+                                "gemm_skinny"))
+            return rc;
+        return hip_status(launch_combine(Y, k, nullptr, w, residual, T, d, K, dtype, y, s),
+                          "combine");
+    }
     if (int rc = hip_status(launch_dispatch(k, ids, T, N, K, counts, offsets, row_token, inv,
                                             hist, tile_off, tail_list, plan, s), "dispatch"))
         return rc;
-    if (gemm_use_skinny(dtype, T, K, N, d, m)) {
-        if (int rc = hip_status(launch_gemm_skinny(x, W_gate_up, W_down, packed, row_token, offsets, d,
-                                                   N, m, H, Y, s), "gemm_skinny"))
-            return rc;
-    } else {
+    {
         if (int rc = hip_status(launch_gemm_gate_up(x, W_gate_up, row_token, offsets, tile_off,
                                                     big ? tail_list : nullptr, mt, tr, d, N, m,
                                                     dtype, H, s),

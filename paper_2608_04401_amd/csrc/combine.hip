@@ -1,6 +1,6 @@
 // Weighted combine of the expert outputs back to token order (the MoE output is the
 // routing-weighted sum over the token's selected experts, Section 2):
-//   y[t] = [residual[t] +] sum_{j < k_t} w[t, j] * Y[inv[t, j]]
+//   y[t] = [residual[t] +] sum_{j < k_t} w[t, j] * Y[inv[t, j]]   (no inv: Y[t K + j])
 // summed in rank order j = 0, 1, ... with fp32 accumulation (deterministic; no atomics).
 // y may alias residual (each element is read, then written, by the same thread).
 // One block per token; each thread owns 8 (bf16) or 4 (fp32) consecutive columns, so every
@@ -31,10 +31,10 @@ __global__ __launch_bounds__(256) void combine_bf16(const bf16_t* __restrict__ Y
             for (int i = 0; i < 8; ++i) acc[i] = 0.f;
         }
         for (int j = 0; j < kt && j < K; ++j) {
-            const int r = inv[t * K + j];
+            const int64_t r = inv ? inv[t * K + j] : t * K + j;
             if (r < 0) continue;
             const float wj = w[t * K + j];
-            const uint4 q = *reinterpret_cast<const uint4*>(Y + (int64_t)r * d + c);
+            const uint4 q = *reinterpret_cast<const uint4*>(Y + r * d + c);
             const bf16_t* h = reinterpret_cast<const bf16_t*>(&q);
 #pragma unroll
             for (int i = 0; i < 8; ++i) acc[i] = fmaf(wj, bf16_to_f32(h[i]), acc[i]);
@@ -59,10 +59,10 @@ __global__ __launch_bounds__(256) void combine_f32(const float* __restrict__ Y,
         float4 acc = residual ? *reinterpret_cast<const float4*>(residual + t * d + c)
                               : make_float4(0.f, 0.f, 0.f, 0.f);
         for (int j = 0; j < kt && j < K; ++j) {
-            const int r = inv[t * K + j];
+            const int64_t r = inv ? inv[t * K + j] : t * K + j;
             if (r < 0) continue;
             const float wj = w[t * K + j];
-            const float4 q = *reinterpret_cast<const float4*>(Y + (int64_t)r * d + c);
+            const float4 q = *reinterpret_cast<const float4*>(Y + r * d + c);
             acc.x = fmaf(wj, q.x, acc.x);
             acc.y = fmaf(wj, q.y, acc.y);
             acc.z = fmaf(wj, q.z, acc.z);

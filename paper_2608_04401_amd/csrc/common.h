@@ -89,15 +89,17 @@ hipError_t launch_gemm_down(const void* H, const void* Wd, const int* offsets,
 
 // decode-sized batches: weight-streaming gate/up (+SwiGLU) and down GEMMs, both launched
 bool gemm_use_skinny(int dtype, int64_t T, int K, int N, int d, int m);
-// packed: the weights' packed copy (launch_pack_experts) or nullptr for the row-major ones
+// rows are assignment slots t K + j found from the routing (k, ids) itself (no dispatch):
+// H [T K, m], Y [T K, d]; counts (optional): assignments per expert.  packed: the weights'
+// packed copy (launch_pack_experts) or nullptr for the row-major ones
 hipError_t launch_gemm_skinny(const void* x, const void* Wgu, const void* Wd, const void* packed,
-                              const int* row_token, const int* offsets, int d, int N, int m,
-                              void* H, void* Y, hipStream_t s);
+                              const int* k, const int* ids, int64_t T, int K, int d, int N,
+                              int m, void* H, void* Y, int* counts, hipStream_t s);
 // the packed copy of bf16 W_gate_up [N, 2m, d] and W_down [N, d, m] (same total size)
 hipError_t launch_pack_experts(const void* Wgu, const void* Wd, int N, int d, int m,
                                void* packed, hipStream_t s);
 
-// combine: y[t] = residual[t] + sum_j w[t, j] Y[inv[t, j]]
+// combine: y[t] = residual[t] + sum_j w[t, j] Y[inv[t, j]]  (inv == nullptr: row t K + j)
 hipError_t launch_combine(const void* Y, const int* k, const int* inv, const float* w,
                           const void* residual, int64_t T, int d, int K, int dtype, void* y,
                           hipStream_t s);

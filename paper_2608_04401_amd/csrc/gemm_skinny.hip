@@ -36,25 +36,53 @@ template <int MODE, int MT, bool PACKED>
 __device__ __forceinline__ void skinny_chunk(const bf16_t* const (&wp)[SK_NF],
                                              const bf16_t* const (&xp)[SK_MAXMT], int kd,
                                              int rows, int64_t out_row0, int out_ld,
-                                             int out_col, bf16_t* __restrict__ C, int lane) {
+                                             int out_col, bf16_t* __restrict__ C, int lane,
+                                             const int* slots) {
     f32x4_t acc[MT][SK_NF];
 #pragma unroll
     for (int t = 0; t < MT; ++t)
 #pragma unroll
         for (int f = 0; f < SK_NF; ++f) acc[t][f] = f32x4_t{0.f, 0.f, 0.f, 0.f};
     stream_mma<MT, SK_MAXMT, 3, PACKED>(wp, xp, 0, kd / 64, acc);
-    stream_store<MODE, MT>(acc, rows, out_row0, out_ld, out_col, C, lane);
+    stream_store<MODE, MT>(acc, rows, out_row0, out_ld, out_col, C, lane, slots);
 }
 
-// MODE 0: A = x [T, d] gathered through row_token, W = W_gate_up [N, 2m, d], C = H [rows, m]
-// MODE 1: A = H [rows, m], W = W_down [N, d, m], C = Y [rows, d]
+// The assignment slots s = t K + j (j < k_t) routed to expert e, in increasing order (so in
+// increasing token order, as the dispatch orders an expert's rows), gathered by one wave into
+// its LDS list; returns their number.  T K <= kSlotMax on this path.
+constexpr int kSlotMax = 16 * ELB_MAX_EXPERTS;  // T K <= 16 N
+__device__ __forceinline__ int gather_slots(const int* __restrict__ k,
+                                            const int* __restrict__ ids, int T, int K, int e,
+                                            int* list, int lane) {
+    const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+    int n = 0;
+    for (int base = 0; base < T * K; base += kWave) {
+        const int slot = base + lane;
+        bool hit = false;
+        if (slot < T * K) {
+            const int t = slot / K;
+            hit = ids[slot] == e && slot - t * K < k[t];
+        }
+        const uint64_t b = __ballot(hit);
+        if (hit) list[n + __popcll(b & below)] = slot;
+        n += __popcll(b);
+    }
+    return n;
+}
+
+// MODE 0: A = x [T, d], W = W_gate_up [N, 2m, d], C = H [T K, m]
+// MODE 1: A = H [T K, m], W = W_down [N, d, m], C = Y [T K, d]
+// Rows are assignment slots t K + j, found by each wave from the routing itself (k, ids):
+// no dispatch pass; every expert's waves write their slots' rows of H and Y, and the combine
+// reads row t K + j.  counts (optional): assignments per expert, by each expert's first task.
 // PACKED: W is the packed copy of those weights (elb_pack_expert_weights)
 template <int MODE, bool PACKED>
 // (2 waves per SIMD: the register ring of three stages fits in 256 registers)
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) void gemm_skinny(
-    const bf16_t* __restrict__ A, const int* __restrict__ row_token,
-    const bf16_t* __restrict__ W, const int* __restrict__ offsets, int N, int d, int m,
-    bf16_t* __restrict__ C) {
+    const bf16_t* __restrict__ A, const int* __restrict__ k, const int* __restrict__ ids,
+    int T, int K, const bf16_t* __restrict__ W, int N, int d, int m, bf16_t* __restrict__ C,
+    int* __restrict__ counts) {
+    __shared__ int slots[4][kSlotMax];
     const int lane = threadIdx.x & 63;
     const int per_e = (MODE == 0) ? m / 32 : d / 64;  // tasks per expert
     const int nblk = (N * per_e + 3) / 4;
@@ -65,8 +93,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     const int task = L * 4 + (threadIdx.x >> 6);
     if (task >= N * per_e) return;  // wave-uniform; the kernel has no barriers
     const int e = task / per_e, c = task - e * per_e;
-    const int row0 = offsets[e];
-    const int nrows = offsets[e + 1] - row0;
+    int* list = slots[threadIdx.x >> 6];
+    const int nrows = gather_slots(k, ids, T, K, e, list, lane);
+    if (counts && c == 0 && lane == 0) counts[e] = nrows;
     if (nrows <= 0) return;
 
     const int kd = (MODE == 0) ? d : m;
@@ -76,13 +105,12 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
         const int rows = nrows - cb < 16 * SK_MAXMT ? nrows - cb : 16 * SK_MAXMT;
         const bf16_t* wp[SK_NF];
         const bf16_t* xp[SK_MAXMT];
-        stream_task<MODE, SK_MAXMT>(A, row_token, W, e, c, row0 + cb, rows, d, m, lane, wp, xp);
+        stream_task<MODE, SK_MAXMT>(A, nullptr, W, e, c, cb, rows, d, m, lane, wp, xp, list, K);
         if (PACKED) stream_task_packed<MODE>(W, e, c, d, m, lane, wp);
-        const int64_t orow = row0 + cb;
         if (rows <= 16)
-            skinny_chunk<MODE, 1, PACKED>(wp, xp, kd, rows, orow, out_ld, out_col, C, lane);
+            skinny_chunk<MODE, 1, PACKED>(wp, xp, kd, rows, cb, out_ld, out_col, C, lane, list);
         else
-            skinny_chunk<MODE, 2, PACKED>(wp, xp, kd, rows, orow, out_ld, out_col, C, lane);
+            skinny_chunk<MODE, 2, PACKED>(wp, xp, kd, rows, cb, out_ld, out_col, C, lane, list);
     }
 }
 
@@ -128,38 +156,39 @@ unsigned blocks_for(int tasks) { return (unsigned)(((tasks + 3) / 4 + 7) / 8 * 8
 
 bool gemm_use_skinny(int dtype, int64_t T, int K, int N, int d, int m) {
     // at most 16 rows per expert on average: far below the bf16 ridge point (~300 rows), so
-    // the weight stream bounds the GEMMs
+    // the weight stream bounds the GEMMs (T K <= 16 N <= kSlotMax, the waves' slot lists)
     return dtype == ELB_BF16 && T > 0 && T * K <= (int64_t)16 * N && m % 32 == 0 &&
            d % 64 == 0 && m % 64 == 0;
 }
 
 hipError_t launch_gemm_skinny(const void* x, const void* Wgu, const void* Wd, const void* packed,
-                              const int* row_token, const int* offsets, int d, int N, int m,
-                              void* H, void* Y, hipStream_t s) {
+                              const int* k, const int* ids, int64_t T, int K, int d, int N,
+                              int m, void* H, void* Y, int* counts, hipStream_t s) {
     const bf16_t* pgu = (const bf16_t*)packed;
     const bf16_t* pd = pgu ? pgu + (int64_t)N * 2 * m * d : nullptr;
+    const int t = (int)T;
     {
         ProfileScope prof("gemm_gate_up_skinny", s);
         if (pgu)
             hipLaunchKernelGGL((gemm_skinny<0, true>), dim3(blocks_for(N * (m / 32))), dim3(256),
-                               0, s, (const bf16_t*)x, row_token, pgu, offsets, N, d, m,
-                               (bf16_t*)H);
+                               0, s, (const bf16_t*)x, k, ids, t, K, pgu, N, d, m, (bf16_t*)H,
+                               counts);
         else
             hipLaunchKernelGGL((gemm_skinny<0, false>), dim3(blocks_for(N * (m / 32))),
-                               dim3(256), 0, s, (const bf16_t*)x, row_token,
-                               (const bf16_t*)Wgu, offsets, N, d, m, (bf16_t*)H);
+                               dim3(256), 0, s, (const bf16_t*)x, k, ids, t, K,
+                               (const bf16_t*)Wgu, N, d, m, (bf16_t*)H, counts);
     }
     if (hipError_t e = hipGetLastError(); e != hipSuccess) return e;
     {
         ProfileScope prof("gemm_down_skinny", s);
         if (pd)
             hipLaunchKernelGGL((gemm_skinny<1, true>), dim3(blocks_for(N * (d / 64))), dim3(256),
-                               0, s, (const bf16_t*)H, (const int*)nullptr, pd, offsets, N, d,
-                               m, (bf16_t*)Y);
+                               0, s, (const bf16_t*)H, k, ids, t, K, pd, N, d, m, (bf16_t*)Y,
+                               (int*)nullptr);
         else
             hipLaunchKernelGGL((gemm_skinny<1, false>), dim3(blocks_for(N * (d / 64))),
-                               dim3(256), 0, s, (const bf16_t*)H, (const int*)nullptr,
-                               (const bf16_t*)Wd, offsets, N, d, m, (bf16_t*)Y);
+                               dim3(256), 0, s, (const bf16_t*)H, k, ids, t, K,
+                               (const bf16_t*)Wd, N, d, m, (bf16_t*)Y, (int*)nullptr);
     }
     return hipGetLastError();
 }

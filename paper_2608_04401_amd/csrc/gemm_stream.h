@@ -32,13 +32,16 @@ constexpr int SK_NF = 4;  // 16-row weight fragments per task (64 weight rows)
 
 // Lane addresses of a task: wp[f] in weight fragment f (row l16, k offset kq) and xp[t] in
 // token tile t (row l16 of rows [row0, row0 + rows), clamped to a valid row, k offset kq).
+// slots (optional): the rows are assignment slots t K + j listed at slots[row0 + r] (gate/up
+// reads token t's x row, down reads row slot of H) instead of the dispatch's row order.
 template <int MODE, int MAXMT>
 __device__ __forceinline__ void stream_task(const bf16_t* __restrict__ A,
                                             const int* __restrict__ row_token,
                                             const bf16_t* __restrict__ W, int e, int c,
                                             int row0, int rows, int d, int m, int lane,
                                             const bf16_t* (&wp)[SK_NF],
-                                            const bf16_t* (&xp)[MAXMT]) {
+                                            const bf16_t* (&xp)[MAXMT],
+                                            const int* slots = nullptr, int K = 1) {
     const int kd = (MODE == 0) ? d : m;
     const int l16 = lane & 15, kq = (lane >> 4) * 8;
 #pragma unroll
@@ -51,8 +54,13 @@ __device__ __forceinline__ void stream_task(const bf16_t* __restrict__ A,
     for (int t = 0; t < MAXMT; ++t) {
         int r = 16 * t + l16;
         r = r < rows ? r : rows - 1;  // rows past the chunk: a valid row, never stored
-        const int64_t src = (MODE == 0) ? (int64_t)row_token[row0 + r] * d
-                                        : (int64_t)(row0 + r) * m;
+        int64_t src;
+        if (slots) {
+            const int slot = slots[row0 + r];
+            src = (MODE == 0) ? (int64_t)(slot / K) * d : (int64_t)slot * m;
+        } else {
+            src = (MODE == 0) ? (int64_t)row_token[row0 + r] * d : (int64_t)(row0 + r) * m;
+        }
         xp[t] = A + src + kq;
     }
 }
@@ -144,17 +152,20 @@ __device__ __forceinline__ void stream_mma(const bf16_t* const (&wp)[SK_NF],
 // Store a task's outputs for token rows [0, rows): the lane holds token row (lane & 15) of
 // each tile and, per fragment f, the 4 consecutive output columns 16 f + (lane >> 4) * 4 + i
 // of the task (gate/up: SwiGLU of fragment f and f + 2, f < 2).  bf16 out, 8-byte stores.
+// slots (optional): output row of r is slots[out_row0 + r] instead of out_row0 + r.
 template <int MODE, int MT>
 __device__ __forceinline__ void stream_store(const f32x4_t (&acc)[MT][SK_NF], int rows,
                                              int64_t out_row0, int out_ld, int out_col,
-                                             bf16_t* __restrict__ C, int lane) {
+                                             bf16_t* __restrict__ C, int lane,
+                                             const int* slots = nullptr) {
     const int l16 = lane & 15;
     const int cq = (lane >> 4) * 4;
 #pragma unroll
     for (int t = 0; t < MT; ++t) {
         const int r = 16 * t + l16;
         if (r >= rows) continue;
-        bf16_t* dst = C + (out_row0 + r) * (int64_t)out_ld + out_col + cq;
+        const int64_t orow = slots ? (int64_t)slots[out_row0 + r] : out_row0 + r;
+        bf16_t* dst = C + orow * (int64_t)out_ld + out_col + cq;
         if (MODE == 0) {
 #pragma unroll
             for (int f = 0; f < 2; ++f) {  // fragments 0, 1: gate; 2, 3: the matching up
