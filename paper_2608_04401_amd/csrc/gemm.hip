@@ -382,19 +382,22 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
     // would otherwise wait for every copy in flight before each LDS read.  Waits are explicit
     // (ELB_WAIT_VMCNT); M0 carries the LDS destination and is set in the same statement.
     // Each call is 8 copy instructions per wave.
+    // copy instruction i (of 8) of a unit; weights carry the non-temporal hint (streamed, read
+    // by the expert's few M-tiles only)
+    auto issue_one = [&](const bf16_t* src, const uint32_t (&off)[8], int unit, int k0, bool nt,
+                         int i) {
+        const uint32_t la = lds0 + (uint32_t)unit * (UNIT * 2) + i * 1024;
+        const uint32_t va = (off[i] + k0) * 2u;
+        if (nt)
+            asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2 nt"
+                         :: "s"(la), "v"(va), "s"(src) : "memory", "m0");
+        else
+            asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2"
+                         :: "s"(la), "v"(va), "s"(src) : "memory", "m0");
+    };
     auto issue = [&](const bf16_t* src, const uint32_t (&off)[8], int unit, int k0, bool nt) {
-        const uint32_t base = lds0 + (uint32_t)unit * (UNIT * 2);
 #pragma unroll
-        for (int i = 0; i < 8; ++i) {
-            const uint32_t la = base + i * 1024;
-            const uint32_t va = (off[i] + k0) * 2u;  // byte offset
-            if (nt)  // weights: streamed, read by the expert's few M-tiles only
-                asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2 nt"
-                             :: "s"(la), "v"(va), "s"(src) : "memory", "m0");
-            else
-                asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2"
-                             :: "s"(la), "v"(va), "s"(src) : "memory", "m0");
-        }
+        for (int i = 0; i < 8; ++i) issue_one(src, off, unit, k0, nt, i);
     };
 
     // fragment rows (element offsets inside a stage)
@@ -452,12 +455,13 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
     };
 
     // Pipeline: the B half of k-tile t lives in unit 2t mod 5, its A half in unit 2t + 1
-    // mod 5.  After the third k16-step of tile t each wave waits for its own copies of tile
-    // t + 1 and for its own LDS reads; the barrier then makes tile t + 1 visible to every wave
-    // and frees tile t's two units (every read of them has completed), which receive the A
-    // half of tile t + 2 and the B half of tile t + 3 before the fourth k16-step runs.  Copies
-    // complete in order and each half is 8 instructions per wave; the only copies issued after
-    // tile t + 1's are those of B(t + 2), so the wait is vmcnt <= 8 (0 near the end).
+    // mod 5.  Once the fourth k16-step's fragments of tile t are read (after the second
+    // step's MFMAs) each wave waits for its own copies of tile t + 1 and for its own LDS
+    // reads; the barrier then makes tile t + 1 visible to every wave and frees tile t's two
+    // units (every read of them has completed), which receive the A half of tile t + 2 and the
+    // B half of tile t + 3 while the third and fourth steps' MFMAs run.  Copies complete in
+    // order and each half is 8 instructions per wave; the only copies issued after tile
+    // t + 1's are those of B(t + 2), so the wait is vmcnt <= 8 (0 near the end).
     // A bare s_barrier, not __syncthreads(): the latter's fence would make the compiler drain
     // every copy in flight.
     const int nk = Kd / TK;  // >= 1
@@ -488,16 +492,37 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
         load(fa0, fb0, ua, ub, 2);
         mma(fa1, fb1, true);
         load(fa1, fb1, ua, ub, 3);
-        mma(fa0, fb0, true);
         __builtin_amdgcn_sched_barrier(0);
         if (t + 2 < nk) ELB_WAIT_VMCNT(8);
         else ELB_WAIT_VMCNT(0);
         asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
-        if (t + 2 < nk) issue(A, a_off, ub, (t + 2) * TK, false);   // A(t + 2) -> unit 2t
-        if (t + 3 < nk) issue(B, b_off, ua, (t + 3) * TK, true);   // B(t + 3) -> unit 2t + 1
-        __builtin_amdgcn_sched_barrier(0);
-        load(fa0, fb0, ua1, ub1, 0);
-        mma(fa1, fb1, true);
+        // k16-steps 2 and 3 (32 MFMAs), with one of the 16 copy instructions of A(t + 2) and
+        // B(t + 3) after every other MFMA: a copy that cannot issue at once then holds up one
+        // MFMA slot, not a burst of them.  The next tile's step-0 reads go between the steps.
+#pragma unroll
+        for (int q = 0; q < 32; ++q) {
+            const int mi = (q & 15) >> 2, ni = q & 3;
+            if (q < 16)
+                acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb0[ni], fa0[mi],
+                                                                      acc[mi][ni], 0, 0, 0);
+            else
+                acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb1[ni], fa1[mi],
+                                                                      acc[mi][ni], 0, 0, 0);
+            __builtin_amdgcn_sched_barrier(0);
+            if (q == 15) {
+                load(fa0, fb0, ua1, ub1, 0);
+                __builtin_amdgcn_sched_barrier(0);
+            }
+            if ((q & 1) == 1) {
+                const int i = q >> 1;
+                if (i < 8) {
+                    if (t + 2 < nk) issue_one(A, a_off, ub, (t + 2) * TK, false, i);  // -> unit 2t
+                } else {
+                    if (t + 3 < nk) issue_one(B, b_off, ua, (t + 3) * TK, true, i - 8);
+                }
+                __builtin_amdgcn_sched_barrier(0);
+            }
+        }
         ub = ub1;
         ua = ua1;
     }
