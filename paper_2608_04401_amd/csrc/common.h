@@ -28,6 +28,12 @@ __device__ __forceinline__ bf16_t f32_to_bf16(float f) {
 
 constexpr int kWave = 64;
 
+// LDS pointers as 32-bit LDS addresses (for the M0 operand of global_load_lds_dwordx4)
+typedef __attribute__((address_space(3))) void lds_void_t;
+
+// s_waitcnt vmcnt(n) (expcnt and lgkmcnt not waited on); n a compile-time constant
+#define ELB_WAIT_VMCNT(n) __builtin_amdgcn_s_waitcnt(((n) & 15) | (((n) >> 4) << 14) | 0x0F70)
+
 // ---- kernel launchers (defined in the .hip files); each returns hipGetLastError() ----
 
 // routing: logits [T, N] -> k [T], ids [T, K], w [T, K]

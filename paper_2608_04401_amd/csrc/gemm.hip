@@ -237,15 +237,12 @@ constexpr int LBM = 256, LBN = 256;
 
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
-typedef __attribute__((address_space(3))) void lds_void_t;
 
 // physical 16-byte chunk of logical chunk c (0..7) in a 128-byte LDS row r
 __device__ __forceinline__ int swz8(int r, int c) {
     return c ^ (((r >> 1) ^ ((r & 1) << 2)) & 7);
 }
 
-// s_waitcnt vmcnt(n) (expcnt and lgkmcnt not waited on)
-#define ELB_WAIT_VMCNT(n) __builtin_amdgcn_s_waitcnt(((n) & 15) | (((n) >> 4) << 14) | 0x0F70)
 
 // two floats -> two bf16 (round to nearest even) in one v_cvt_pk_bf16_f32
 typedef __bf16 bf16x2_vt __attribute__((ext_vector_type(2)));

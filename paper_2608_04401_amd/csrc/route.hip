@@ -2,9 +2,17 @@
 // per-token arithmetic and its reading of Section 2, Section 2.1 and Appendix A.1
 // Algorithm 1 are in route_lane.h).
 //
-// GPU design (CDNA4, wave64): one LANE per token.  A wave stages its 64 tokens' logits
-// (64 * N contiguous floats) through LDS with coalesced loads, then every lane routes its
-// token from its staged row.
+// GPU design (CDNA4, wave64): one LANE per token; a wave owns 64 consecutive tokens.
+//  - route_dma_kernel (N = 16, 32, 64, 16-byte aligned logits): the wave's 64 N logits are
+//    copied straight from HBM into its LDS tile (global_load_lds_dwordx4, no registers) in
+//    two parts of N / 2 columns each (whole 128-byte lines of every row), issued at once;
+//    each lane sorts its row's first half as soon as it has landed (the sorting network run
+//    in part order, sortnet.h PhasedNet) while the second is still in flight.  The tile is
+//    swizzled so that 16 lanes reading their own rows hit 16 distinct bank groups.  The
+//    outputs (k, ids, w) are staged in the tile and stored with whole-wave contiguous
+//    16-byte stores.
+//  - route_kernel (any N <= 64): the rows staged through registers into a padded LDS tile;
+//    every lane routes its token from its row and stores its own outputs.
 #include "route_lane.h"
 
 namespace elb {
@@ -36,6 +44,157 @@ __global__ __launch_bounds__(256) void route_kernel(const float* __restrict__ lo
                                 ids, wout);
 }
 
+// ---- route_dma_kernel ----
+
+// LDS DMA layout of a wave's 64 x NP tile: P parts of CP 16-byte chunks per row; chunk cc of
+// part p of row r sits at 16-byte slot p 64 CP + r CP + (cc ^ swz(r)), so that for a fixed
+// chunk 16 consecutive rows fall in 16 distinct groups of 4 banks.
+constexpr int kRouteParts = 2;  // parts of the copy (a power of two)
+
+template <int NP>
+struct DmaTile {
+    static constexpr int C = NP / 4;              // 16-byte chunks per row
+    static constexpr int P = C >= kRouteParts ? kRouteParts : C;  // parts
+    static constexpr int CP = C / P;              // chunks per row per part
+    static constexpr int B = NP / P;              // floats per row per part
+    static constexpr int RPG = 16 / CP;           // rows per swizzle period
+    __device__ static int swz(int r) { return (r / RPG) % CP; }
+    // float index of value c (0 <= c < NP) of row r
+    __device__ static int at(int r, int c) {
+        const int p = c / B, cc = (c % B) / 4;
+        return ((p * 64 * CP + r * CP + (cc ^ swz(r))) << 2) + (c & 3);
+    }
+};
+
+template <int NP, int P, int G, int... I>
+__device__ __forceinline__ void sort_group(float* key, std::integer_sequence<int, I...>) {
+    (compare_exchange<NP, PhasedHolder<NP, P>::net.idx[G][I]>(key), ...);
+}
+
+// read part p of row `lane` into key[p B .. p B + B) (and okey), then sort that part
+template <int NP, int G>
+__device__ __forceinline__ void load_sort_part(const float* tile, int lane, float* key,
+                                               float* okey) {
+    using L = DmaTile<NP>;
+#pragma unroll
+    for (int cc = 0; cc < L::CP; ++cc) {
+        const float4 v = *reinterpret_cast<const float4*>(
+            tile + ((G * 64 * L::CP + lane * L::CP + (cc ^ L::swz(lane))) << 2));
+        const int c0 = G * L::B + cc * 4;
+        okey[c0 + 0] = order_key(v.x);
+        okey[c0 + 1] = order_key(v.y);
+        okey[c0 + 2] = order_key(v.z);
+        okey[c0 + 3] = order_key(v.w);
+#pragma unroll
+        for (int q = 0; q < 4; ++q) key[c0 + q] = okey[c0 + q];
+    }
+    sort_group<NP, L::P, G>(
+        key, std::make_integer_sequence<int, PhasedHolder<NP, L::P>::net.cnt[G]>{});
+}
+
+// N == NP in {16, 32, 64}; logits 16-byte aligned.  vst: ids and w 16-byte aligned (the
+// output stores are then 16 bytes wide).
+template <int NP, int KMAX>
+__global__ __launch_bounds__(256) void route_dma_kernel(const float* __restrict__ logits,
+                                                        int64_t T, int K, float eps, int mode,
+                                                        int renorm, int vst, XTable xt,
+                                                        int* __restrict__ kout,
+                                                        int* __restrict__ ids,
+                                                        float* __restrict__ wout) {
+    using L = DmaTile<NP>;
+    constexpr int TILE = 64 * NP;               // floats of the logit tile
+    constexpr int STG = 64 * (KMAX + 1) * 2;    // floats of the staged outputs
+    constexpr int WS = TILE > STG ? TILE : STG;
+    __shared__ __attribute__((aligned(1024))) float lds[4 * WS];
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // uniform: scalar bases
+    const int64_t t0 = ((int64_t)blockIdx.x * 4 + wv) * kWave;
+    if (t0 >= T) return;  // wave-uniform; the kernel has no block barrier
+    const int rows = (int)((T - t0) < kWave ? (T - t0) : kWave);
+    float* tile = lds + wv * WS;
+
+    // ---- copy the tile: part p, instruction j of CP; lane -> (row, slot) of its 16 bytes ----
+    const float* src = logits + t0 * NP;
+    const uint32_t lds0 = (uint32_t)(uintptr_t)(lds_void_t*)tile;
+#pragma unroll
+    for (int p = 0; p < L::P; ++p)
+#pragma unroll
+        for (int j = 0; j < L::CP; ++j) {
+            const int local = j * 64 + lane;
+            const int r = local / L::CP;
+            const int cc = (local % L::CP) ^ L::swz(r);
+            const int rs = r < rows ? r : rows - 1;  // rows past T: a valid row, never used
+            const uint32_t va = (uint32_t)(rs * NP + (p * L::CP + cc) * 4) * 4u;
+            const uint32_t la = __builtin_amdgcn_readfirstlane(lds0 + (p * 64 * L::CP + j * 64) * 16);
+            asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2"
+                         :: "s"(la), "v"(va), "s"(src) : "memory", "m0");
+        }
+
+    // ---- each part: wait for its copies (they complete in order), read the row's part, sort
+    float key[NP], okey[NP];
+#define ELB_PART(G)                                                                      \
+    if constexpr (G < L::P) {                                                            \
+        __builtin_amdgcn_sched_barrier(0);                                               \
+        ELB_WAIT_VMCNT((L::P - 1 - (G)) * L::CP);                                     \
+        __builtin_amdgcn_sched_barrier(0);                                               \
+        load_sort_part<NP, G>(tile, lane, key, okey);                                    \
+    }
+    ELB_PART(0)
+    ELB_PART(1)
+    ELB_PART(2)
+    ELB_PART(3)
+#undef ELB_PART
+    sort_group<NP, L::P, L::P>(
+        key, std::make_integer_sequence<int, PhasedHolder<NP, L::P>::net.cnt[L::P]>{});
+
+    float u[NP], S;
+    const int k = sorted_elbow<NP, true, KMAX>(key, NP, K, eps, mode, xt, u, S);
+    if (lane < rows) kout[t0 + lane] = k;
+
+    // ---- select; outputs staged in the tile (every read of it precedes, in program order,
+    // every write below, and a wave's LDS operations complete in order) ----
+    int* const stg_i = reinterpret_cast<int*>(tile);
+    float* const stg_w = tile + 64 * (KMAX + 1);
+    const int ld = K + 1;
+    select_emit<NP, true, KMAX>(
+        key, okey, [&](int c) { return order_key(tile[L::at(lane, c)]); }, NP, K, k, u, S,
+        renorm, [&](int j, int id, float w) {
+            stg_i[lane * ld + j] = id;
+            stg_w[lane * ld + j] = w;
+        });
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+
+    // ---- store the wave's rows * K ids and weights: lane l takes elements 4 l .. 4 l + 3 of
+    // every 256 (one contiguous KB per store instruction) ----
+    const int total = rows * K;
+    int* const gi = ids + t0 * K;
+    float* const gw = wout + t0 * K;
+    for (int e0 = 4 * lane; e0 < total; e0 += 256) {
+        int vi[4];
+        float vw[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const int e = e0 + q < total ? e0 + q : total - 1;
+            const int tok = e / K, j = e - tok * K;
+            vi[q] = stg_i[tok * ld + j];
+            vw[q] = stg_w[tok * ld + j];
+        }
+        if (vst && e0 + 4 <= total) {
+            *reinterpret_cast<int4*>(gi + e0) = make_int4(vi[0], vi[1], vi[2], vi[3]);
+            *reinterpret_cast<float4*>(gw + e0) = make_float4(vw[0], vw[1], vw[2], vw[3]);
+        } else {
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+                if (e0 + q < total) {
+                    gi[e0 + q] = vi[q];
+                    gw[e0 + q] = vw[q];
+                }
+        }
+    }
+}
+
 template <int NP, bool FULL, int KMAX>
 hipError_t launch_np(const float* logits, int64_t T, int N, const elb_route_params& p, int* k,
                      int* ids, float* w, hipStream_t s) {
@@ -44,6 +203,14 @@ hipError_t launch_np(const float* logits, int64_t T, int N, const elb_route_para
     const unsigned blocks = (unsigned)((waves + 3) / 4);
     const int vec4 = ((uintptr_t)logits % 16) == 0;
     ProfileScope prof("route", s);
+    if constexpr (FULL && NP >= 16) {
+        if (vec4) {
+            const int vst = ((uintptr_t)ids % 16) == 0 && ((uintptr_t)w % 16) == 0;
+            hipLaunchKernelGGL((route_dma_kernel<NP, KMAX>), dim3(blocks), dim3(256), 0, s,
+                               logits, T, p.K, p.eps, p.mode, p.renormalize, vst, xt, k, ids, w);
+            return hipGetLastError();
+        }
+    }
     hipLaunchKernelGGL((route_kernel<NP, FULL, KMAX>), dim3(blocks), dim3(256), 0, s, logits, T, N, p.K,
                        p.eps, p.mode, p.renormalize, vec4, xt, k, ids, w);
     return hipGetLastError();

@@ -34,6 +34,10 @@ template <int NP>
 struct NetHolder {
     static constexpr OddEvenMergeNet<NP> net{};
 };
+template <int NP, int P>
+struct PhasedHolder {
+    static constexpr PhasedNet<NP, P> net{};
+};
 
 // Sort key of a logit: the value itself, made canonical by an add of +0 (which also turns
 // -0 into +0), so that min/max compile to single v_min_f32/v_max_f32.  Non-NaN inputs.
@@ -108,29 +112,17 @@ __device__ __forceinline__ void stage_rows(const float* __restrict__ src, int N,
     }
 }
 
-// Token t's routing from row[0..N) (LDS).  FULL: N == NP, so every "position < N" test is
-// static; KMAX: a bound on K (8 or 16).  Writes k[t], ids[t, 0..K), w[t, 0..K).
-template <int NP, bool FULL, int KMAX>
-__device__ __forceinline__ void route_token(const float* row, int N, int K, float eps,
-                                            int mode, int renorm, const XTable& xt, int64_t t,
-                                            int* __restrict__ kout, int* __restrict__ ids,
-                                            float* __restrict__ wout) {
-    constexpr int KM = NP < KMAX ? NP : KMAX;
-    const int Nn = FULL ? NP : N;
-    // ---- keys of the token's logits (pads are -inf and sort last) ----
-    const float kNegInf = -INFINITY;
-    float key[NP], okey[NP];
-#pragma unroll
-    for (int c = 0; c < NP; ++c) {
-        okey[c] = (c < Nn) ? order_key(row[c]) : kNegInf;
-        key[c] = okey[c];
-    }
-    sort_desc<NP>(key, std::make_integer_sequence<int, NetHolder<NP>::net.n>{});
+// ---- the per-token steps, shared by every kernel that routes in one lane ----
 
-    // ---- u_i = exp(l_(i) - l_(0)) (0 for pads); S = sum u; u_min = u_(N-1) ----
+// u_i = exp(l_(i) - l_(0)) in rank order (0 for pads), S = sum u in rank order, and the
+// elbow's k (K in top-K mode) from the sorted keys.
+template <int NP, bool FULL, int KMAX>
+__device__ __forceinline__ int sorted_elbow(const float (&key)[NP], int Nn, int K, float eps,
+                                            int mode, const XTable& xt, float (&u)[NP],
+                                            float& S) {
+    constexpr int KM = NP < KMAX ? NP : KMAX;
     const float lmax = key[0];
-    float u[NP];
-    float S = 0.f;
+    S = 0.f;
 #pragma unroll
     for (int i = 0; i < NP; ++i) {
         u[i] = __builtin_amdgcn_exp2f((key[i] - lmax) * kLog2e);
@@ -141,7 +133,6 @@ __device__ __forceinline__ void route_token(const float* row, int N, int K, floa
 #pragma unroll
         for (int i = 0; i < NP; ++i) umin = (i == Nn - 1) ? u[i] : umin;
     }
-
     int k = K;
     if (mode == ELB_MODE_ELBOW) {
         // scaled deviation (1 - u_i) - x'_i (1 - u_min + eps S); D_0 == 0 exactly.  The first
@@ -166,8 +157,20 @@ __device__ __forceinline__ void route_token(const float* row, int N, int K, floa
         }
         k = (tail > best) ? K : e + 1;
     }
+    return k;
+}
 
-    // ---- ids of the k selected experts: the k largest keys, equal keys by lower id ----
+// The k selected experts (the k largest keys, equal keys by lower id) with their weights,
+// handed to emit(rank, id, w) in no particular order of rank, then emit(j, -1, 0) for
+// k <= j < K.  okey: the token's keys by expert id; key_of(c): expert c's key re-read from
+// memory (c is not a compile-time constant there).
+template <int NP, bool FULL, int KMAX, class KeyOf, class Emit>
+__device__ __forceinline__ void select_emit(const float (&key)[NP], const float (&okey)[NP],
+                                            KeyOf&& key_of, int Nn, int K, int k,
+                                            const float (&u)[NP], float S, int renorm,
+                                            Emit&& emit) {
+    constexpr int KM = NP < KMAX ? NP : KMAX;
+    const float lmax = key[0];
     // tau = key of rank k-1; g = ranks < k with a key above tau; the rest of the k come
     // from the experts whose key equals tau, lowest ids first.
     float tau = key[0];
@@ -210,7 +213,7 @@ __device__ __forceinline__ void route_token(const float* row, int N, int K, floa
             else { sel_hi |= 1u << (b - 32); eq_hi &= ~(1u << (b - 32)); }
         }
     }
-    // the selected experts in id order, with their keys (re-read from the staged row)
+    // the selected experts in id order, with their keys
     int cid[KM];
     float ck[KM];
 #pragma unroll
@@ -218,11 +221,10 @@ __device__ __forceinline__ void route_token(const float* row, int N, int K, floa
         const int b = lowest_bit(sel_lo, sel_hi);
         const bool on = r < k;
         cid[r] = b;
-        ck[r] = on ? order_key(row[b]) : -INFINITY;
+        ck[r] = on ? key_of(b) : -INFINITY;
         if (b < 32) sel_lo &= sel_lo - 1;
         else sel_hi &= sel_hi - 1;
     }
-    // rank of each in descending order (equal keys: lower id, i.e. lower r, first)
     float denom = S;
     if (renorm) {
         float sel = 0.f;
@@ -232,7 +234,7 @@ __device__ __forceinline__ void route_token(const float* row, int N, int K, floa
         denom = sel;
     }
     const float inv = 1.0f / denom;
-    kout[t] = k;
+    // rank of each in descending order (equal keys: lower id, i.e. lower r, first)
 #pragma unroll
     for (int r = 0; r < KM; ++r) {
         if (r < k) {
@@ -242,18 +244,39 @@ __device__ __forceinline__ void route_token(const float* row, int N, int K, floa
                 if (q < r) rank += (q < k && ck[q] >= ck[r]) ? 1 : 0;
                 if (q > r) rank += (q < k && ck[q] > ck[r]) ? 1 : 0;
             }
-            ids[t * K + rank] = cid[r];
-            wout[t * K + rank] =
-                __builtin_amdgcn_exp2f((ck[r] - lmax) * kLog2e) * inv;
+            emit(rank, cid[r], __builtin_amdgcn_exp2f((ck[r] - lmax) * kLog2e) * inv);
         }
     }
 #pragma unroll
-    for (int j = 0; j < KM; ++j) {
-        if (j >= k && j < K) {
-            ids[t * K + j] = -1;
-            wout[t * K + j] = 0.f;
-        }
+    for (int j = 0; j < KM; ++j)
+        if (j >= k && j < K) emit(j, -1, 0.f);
+}
+
+// Token t's routing from row[0..N) (LDS).  FULL: N == NP, so every "position < N" test is
+// static; KMAX: a bound on K (8 or 16).  Writes k[t], ids[t, 0..K), w[t, 0..K).
+template <int NP, bool FULL, int KMAX>
+__device__ __forceinline__ void route_token(const float* row, int N, int K, float eps,
+                                            int mode, int renorm, const XTable& xt, int64_t t,
+                                            int* __restrict__ kout, int* __restrict__ ids,
+                                            float* __restrict__ wout) {
+    const int Nn = FULL ? NP : N;
+    // ---- keys of the token's logits (pads are -inf and sort last) ----
+    float key[NP], okey[NP];
+#pragma unroll
+    for (int c = 0; c < NP; ++c) {
+        okey[c] = (c < Nn) ? order_key(row[c]) : -INFINITY;
+        key[c] = okey[c];
     }
+    sort_desc<NP>(key, std::make_integer_sequence<int, NetHolder<NP>::net.n>{});
+    float u[NP], S;
+    const int k = sorted_elbow<NP, FULL, KMAX>(key, Nn, K, eps, mode, xt, u, S);
+    kout[t] = k;
+    select_emit<NP, FULL, KMAX>(
+        key, okey, [&](int c) { return order_key(row[c]); }, Nn, K, k, u, S, renorm,
+        [&](int j, int id, float w) {
+            ids[t * K + j] = id;
+            wout[t * K + j] = w;
+        });
 }
 
 }  // namespace
