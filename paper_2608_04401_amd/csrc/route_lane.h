@@ -279,6 +279,152 @@ __device__ __forceinline__ void route_token(const float* row, int N, int K, floa
         });
 }
 
+// ---- one token by 16 lanes (N = 64): for latency, where few tokens are routed at once ----
+//
+// The same keys, u, S, deviations, first argmax and weights as route_token, bit for bit, with
+// the work spread over 16 consecutive lanes of a wave (lane sl holds ranks 4 sl .. 4 sl + 3):
+// the (key, id) pairs are sorted by a bitonic network whose strides of 4 and more cross lanes
+// (shuffles inside the 16-lane group); S (and the renormalised denominator) is summed in rank
+// order by the group's first lane from the u values left in the token's LDS row; the first
+// argmax and the tail maximum are exact reductions over the group.
+
+// the order-preserving integer image of a canonical fp32 value, and its inverse
+__device__ __forceinline__ int ord_flip32(int i) { return i ^ ((i >> 31) & 0x7fffffff); }
+
+__device__ __forceinline__ int64_t shfl_xor64(int64_t v, int m) {
+    const int lo = __shfl_xor((int)(uint32_t)v, m, 16);
+    const int hi = __shfl_xor((int)(v >> 32), m, 16);
+    return ((int64_t)hi << 32) | (uint32_t)lo;
+}
+
+// row: the token's 64 logits in LDS (overwritten with its u values); every lane of the
+// group calls this (valid: the token exists; only valid groups write)
+template <int KMAX>
+__device__ __forceinline__ void route_token_x16(float* row, int K, float eps, int mode,
+                                                int renorm, const XTable& xt, int64_t t,
+                                                bool valid, int* __restrict__ kout,
+                                                int* __restrict__ ids,
+                                                float* __restrict__ wout) {
+    constexpr int NP = 64;
+    const int sl = threadIdx.x & 15;
+    // ---- (key, id) pairs of positions 4 sl + i: key image high, 63 - id low ----
+    int64_t v[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int c = 4 * sl + i;
+        v[i] = ((int64_t)ord_flip32(__float_as_int(order_key(row[c]))) << 32) |
+               (uint32_t)(NP - 1 - c);
+    }
+    // ---- bitonic sort, descending: position p = 4 sl + i ----
+#pragma unroll
+    for (int k = 2; k <= NP; k <<= 1) {
+#pragma unroll
+        for (int j = k >> 1; j >= 1; j >>= 1) {
+            if (j >= 4) {
+                const int m = j >> 2;  // partner lane sl ^ m, same i
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const int p = 4 * sl + i;
+                    const int64_t w = shfl_xor64(v[i], m);
+                    const bool desc = (p & k) == 0 || k == NP;
+                    const bool lower = (p & j) == 0;
+                    const bool take_max = lower == desc;
+                    const bool gt = w > v[i];
+                    v[i] = (gt == take_max) ? w : v[i];
+                }
+            } else {
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    if (i & j) continue;
+                    const int p = 4 * sl + i;
+                    const bool desc = (p & k) == 0 || k == NP;
+                    const int64_t a = v[i], b = v[i | j];
+                    const bool sw = desc ? (b > a) : (a > b);
+                    v[i] = sw ? b : a;
+                    v[i | j] = sw ? a : b;
+                }
+            }
+        }
+    }
+    float key[4];
+    int id[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        key[i] = __int_as_float(ord_flip32((int)(v[i] >> 32)));
+        id[i] = NP - 1 - (int)(uint32_t)v[i];
+    }
+    const float lmax = __shfl(key[0], 0, 16);
+    float u[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        u[i] = __builtin_amdgcn_exp2f((key[i] - lmax) * kLog2e);
+        row[4 * sl + i] = u[i];  // rank order; the group's logits have all been read
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    // ---- S in rank order (first lane), u_min = u of rank 63 ----
+    float S = 0.f;
+    if (sl == 0) {
+        for (int i = 0; i < NP; ++i) S += row[i];
+    }
+    S = __shfl(S, 0, 16);
+    const float umin = __shfl(u[3], 15, 16);
+    int k = K;
+    if (mode == ELB_MODE_ELBOW) {
+        const float Rp = (1.0f - umin) + eps * S;
+        float bd = (sl == 0) ? 0.f : -INFINITY;  // D_0 == 0 exactly
+        int be = (sl == 0) ? 0 : NP;
+        float tail = -INFINITY;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int r = 4 * sl + i;
+            if (r == 0) continue;
+            const float Di = fmaf(-xt.x[r], Rp, 1.0f - u[i]);
+            if (r < K - 1) {
+                if (Di > bd) {  // strict: ranks rise with i, so the first index wins ties
+                    bd = Di;
+                    be = r;
+                }
+            } else {
+                tail = fmaxf(tail, Di);
+            }
+        }
+#pragma unroll
+        for (int m = 8; m >= 1; m >>= 1) {
+            const float obd = __shfl_xor(bd, m, 16);
+            const int obe = __shfl_xor(be, m, 16);
+            const float ot = __shfl_xor(tail, m, 16);
+            if (obd > bd || (obd == bd && obe < be)) {
+                bd = obd;
+                be = obe;
+            }
+            tail = fmaxf(tail, ot);
+        }
+        k = (tail > bd) ? K : be + 1;
+    }
+    float denom = S;
+    if (renorm) {
+        float sel = 0.f;
+        if (sl == 0) {
+            for (int j = 0; j < KMAX; ++j)
+                if (j < k) sel += row[j];
+        }
+        denom = __shfl(sel, 0, 16);
+    }
+    const float inv = 1.0f / denom;
+    if (!valid) return;
+    if (sl == 0) kout[t] = k;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int r = 4 * sl + i;
+        if (r < K) {
+            ids[t * K + r] = (r < k) ? id[i] : -1;
+            wout[t * K + r] = (r < k) ? u[i] * inv : 0.f;
+        }
+    }
+}
+
 }  // namespace
 
 }  // namespace elb

@@ -110,8 +110,10 @@ __global__ __launch_bounds__(64 * RW) void router_bf16(const bf16_t* __restrict_
 }
 
 // Router GEMM and routing fused: the block's 16 x N logits are summed into LDS and routed
-// there by 16 lanes (route_token, the routing kernel's own per-token code), so the logits
-// need not travel through HBM; they are written out only when `logits` is not null.
+// there, so the logits need not travel through HBM; they are written out only when `logits`
+// is not null.  N = 64: 16 lanes per token (route_token_x16); otherwise one lane per token
+// (route_token, the routing kernel's own per-token code).  Both give the routing kernel's
+// bits.
 template <int NP, bool FULL, int KMAX>
 __global__ __launch_bounds__(64 * RW) void router_route_bf16(
     const bf16_t* __restrict__ x, const bf16_t* __restrict__ Wr, int64_t T, int d, int N,
@@ -131,9 +133,16 @@ __global__ __launch_bounds__(64 * RW) void router_route_bf16(
         if (logits && t < T && n < N) logits[t * N + n] = v;
     }
     __syncthreads();
-    if (threadIdx.x < 16 && t0 + threadIdx.x < T)
-        route_token<NP, FULL, KMAX>(&part[0][threadIdx.x][0], N, K, eps, mode, renorm, xt,
-                                    t0 + threadIdx.x, kout, ids, wout);
+    if constexpr (NP == 64 && FULL) {
+        // 16 lanes per token: wave w routes the block's tokens 4 w .. 4 w + 3
+        const int tr = threadIdx.x >> 4;
+        route_token_x16<KMAX>(&part[0][tr][0], K, eps, mode, renorm, xt, t0 + tr,
+                              t0 + tr < T, kout, ids, wout);
+    } else {
+        if (threadIdx.x < 16 && t0 + threadIdx.x < T)
+            route_token<NP, FULL, KMAX>(&part[0][threadIdx.x][0], N, K, eps, mode, renorm,
+                                        xt, t0 + threadIdx.x, kout, ids, wout);
+    }
 }
 
 __global__ __launch_bounds__(256) void router_f32(const float* __restrict__ x,

@@ -30,7 +30,8 @@ def olmoe():
 # ------------------------------------------------------------------------------ dispatch
 @pytest.mark.parametrize("T,N,K", [(65536, 64, 8), (1000, 64, 8), (777, 5, 3), (64, 8, 8),
                                    (1, 2, 1), (4096, 33, 16), (256, 64, 8), (257, 64, 8),
-                                   (200, 64, 64), (130, 17, 5), (255, 3, 3)])
+                                   (200, 64, 64), (130, 17, 5), (255, 3, 3), (8192, 64, 8),
+                                   (8193, 64, 8), (5000, 64, 64), (8000, 7, 2)])
 def test_dispatch_matches_oracle(T, N, K):
     """T <= 256 runs the single-block dispatch, larger T the three-launch one."""
     lg = synth.planted_logits(T, N, seed=T + N, m_max=min(8, N))
