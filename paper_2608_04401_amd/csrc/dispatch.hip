@@ -19,15 +19,28 @@ namespace elb {
 
 namespace {
 
+// slots j0 .. j0 + 7 of token t's ids (-1 past K): eight independent loads, so a lane waits
+// for memory once per eight slots rather than once per slot
+__device__ __forceinline__ void load_ids8(const int* __restrict__ ids, int64_t t, int K, int j0,
+                                          int (&e8)[8]) {
+#pragma unroll
+    for (int q = 0; q < 8; ++q) e8[q] = (j0 + q < K) ? ids[t * K + j0 + q] : -1;
+}
+
 __device__ __forceinline__ uint64_t token_mask(const int* __restrict__ k,
                                                const int* __restrict__ ids, int64_t t, int N,
                                                int K, bool valid) {
     uint64_t mask = 0;
     if (valid) {
         const int kt = k[t];
-        for (int j = 0; j < K; ++j) {
-            const int e = ids[t * K + j];
-            if (j < kt && (unsigned)e < (unsigned)N) mask |= 1ull << e;
+        for (int j0 = 0; j0 < K; j0 += 8) {
+            int e8[8];
+            load_ids8(ids, t, K, j0, e8);
+#pragma unroll
+            for (int q = 0; q < 8; ++q) {
+                const int e = e8[q];
+                if (j0 + q < kt && (unsigned)e < (unsigned)N) mask |= 1ull << e;
+            }
         }
     }
     return mask;
@@ -136,8 +149,11 @@ __global__ __launch_bounds__(256) void dispatch_scatter(const int* __restrict__ 
     const int64_t g = (int64_t)blockIdx.x * 4 + wv;
     const int64_t t = g * kWave + lane;
     const int64_t groups = (T + kWave - 1) / kWave;
-    // expert list offsets and M-tile offsets: exclusive prefixes over the experts (lane e)
+    // expert list offsets and M-tile offsets: exclusive prefixes over the experts (lane e).
+    // The group's histogram entry is loaded together with the totals (one memory round trip
+    // for both; surplus waves read group 0's, unused).
     const int c = (lane < N) ? counts[lane] : 0;
+    const int hist_mine = (lane < N) ? hist[(int64_t)lane * groups + (g < groups ? g : 0)] : 0;
     bool tail_mine;
     int n_tail;
     const int tiles = plan_tiles(c, lane, N, plan, tail_mine, n_tail);  // whole wave
@@ -166,7 +182,7 @@ __global__ __launch_bounds__(256) void dispatch_scatter(const int* __restrict__ 
     const bool valid = t < T;
     const uint64_t mask = token_mask(k, ids, t, N, K, valid);
     // lane e holds the first row of expert e that belongs to this group
-    const int base_mine = (lane < N) ? off_mine + hist[(int64_t)lane * groups + g] : 0;
+    const int base_mine = (lane < N) ? off_mine + hist_mine : 0;
     const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
     for (int e = 0; e < N; ++e) {
         const bool has = (mask >> e) & 1ull;
@@ -180,11 +196,17 @@ __global__ __launch_bounds__(256) void dispatch_scatter(const int* __restrict__ 
     }
     if (!valid) return;
     const int kt = k[t];
-    for (int j = 0; j < K; ++j) {
-        const int e = ids[t * K + j];
-        int r = -1;
-        if (j < kt && (unsigned)e < (unsigned)N) r = pos[wv][lane][e];
-        inv[t * K + j] = r;
+    for (int j0 = 0; j0 < K; j0 += 8) {
+        int e8[8];
+        load_ids8(ids, t, K, j0, e8);
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+            const int j = j0 + q, e = e8[q];
+            if (j >= K) break;
+            int r = -1;
+            if (j < kt && (unsigned)e < (unsigned)N) r = pos[wv][lane][e];
+            inv[t * K + j] = r;
+        }
     }
 }
 
@@ -265,11 +287,17 @@ __global__ __launch_bounds__(256) void dispatch_small(const int* __restrict__ k,
     }
     if (!valid) return;  // no barrier follows
     const int kt = k[t];
-    for (int j = 0; j < K; ++j) {
-        const int e = ids[(int64_t)t * K + j];
-        int r = -1;
-        if (j < kt && (unsigned)e < (unsigned)N) r = pos[wv][lane][e];
-        inv[(int64_t)t * K + j] = r;
+    for (int j0 = 0; j0 < K; j0 += 8) {
+        int e8[8];
+        load_ids8(ids, t, K, j0, e8);
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+            const int j = j0 + q, e = e8[q];
+            if (j >= K) break;
+            int r = -1;
+            if (j < kt && (unsigned)e < (unsigned)N) r = pos[wv][lane][e];
+            inv[(int64_t)t * K + j] = r;
+        }
     }
 }
 

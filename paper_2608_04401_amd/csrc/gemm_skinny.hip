@@ -56,16 +56,23 @@ __device__ __forceinline__ int gather_slots(const int* __restrict__ k,
                                             int* list, int lane) {
     const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
     int n = 0;
-    for (int base = 0; base < T * K; base += kWave) {
-        const int slot = base + lane;
-        bool hit = false;
-        if (slot < T * K) {
-            const int t = slot / K;
-            hit = ids[slot] == e && slot - t * K < k[t];
+    // four 64-slot chunks per pass, their loads issued together (one memory round trip)
+    for (int base = 0; base < T * K; base += 4 * kWave) {
+        int id4[4], k4[4];
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+            const int slot = base + c * kWave + lane;
+            id4[c] = (slot < T * K) ? ids[slot] : -1;
+            k4[c] = (slot < T * K) ? k[slot / K] : 0;
         }
-        const uint64_t b = __ballot(hit);
-        if (hit) list[n + __popcll(b & below)] = slot;
-        n += __popcll(b);
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+            const int slot = base + c * kWave + lane;
+            const bool hit = id4[c] == e && slot - (slot / K) * K < k4[c];
+            const uint64_t b = __ballot(hit);
+            if (hit) list[n + __popcll(b & below)] = slot;
+            n += __popcll(b);
+        }
     }
     return n;
 }
