@@ -82,7 +82,8 @@ def routing_only(B, torch, T=65536, N=64, K=8, nbuf=32, iters=64):
     p = B.RouteParams(K, 1e-8, B.MODE_ELBOW, 0)
     st = C.c_void_p(torch.cuda.current_stream().cuda_stream)
     for i in range(8):
-        L.elb_route(C.c_void_p(bufs[i].data_ptr()), T, N, C.byref(p), C.c_void_p(k.data_ptr()),
+        L.elb_route(C.c_void_p(bufs[i % nbuf].data_ptr()), T, N, C.byref(p),
+                    C.c_void_p(k.data_ptr()),
                     C.c_void_p(ids.data_ptr()), C.c_void_p(w.data_ptr()), st)
     torch.cuda.synchronize()
     B.elb_profile_read()
@@ -294,6 +295,9 @@ def main():
     ap.add_argument("--no-decode", action="store_true", help="skip the decode-sized layer")
     ap.add_argument("--counters", action="store_true",
                     help="run only the workload of the HBM-traffic counter runs")
+    ap.add_argument("--routing-counters", action="store_true",
+                    help="run only the routing kernel on the routing-only workload (for "
+                         "instruction counter runs)")
     ap.add_argument("--traffic-from", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
                     help="write the gate/up GEMM traffic file from two rocprofv3 counter CSVs")
     ap.add_argument("--traffic-command", default="",
@@ -315,6 +319,9 @@ def main():
         print("no GPU visible", file=sys.stderr)
         sys.exit(1)
     B.lib()
+    if args.routing_counters:
+        routing_only(B, torch, nbuf=4, iters=args.steps)
+        return
     T, d, N, m, K = WORKLOADS[args.workload]
     log("generating %s inputs T=%d d=%d N=%d m=%d" % (args.workload, T, d, N, m))
     L = synth.moe_layer(T, d, N, m, dtype="bf16", seed=0)
