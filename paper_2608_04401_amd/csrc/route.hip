@@ -177,7 +177,9 @@ __global__ __launch_bounds__(256) void route_dma_kernel(const float* __restrict_
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
             const int e = e0 + q < total ? e0 + q : total - 1;
-            const int tok = e / K, j = e - tok * K;
+            // element e is slot j of token tok (K == KMAX: a shift, not a division)
+            const int tok = (K == KMAX) ? e / KMAX : e / K;
+            const int j = e - tok * K;
             vi[q] = stg_i[tok * ld + j];
             vw[q] = stg_w[tok * ld + j];
         }
