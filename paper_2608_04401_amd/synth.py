@@ -122,6 +122,37 @@ def stack_input(T: int = 16384, d: int = 2048, seed=0) -> np.ndarray:
     return round_bf16(_normal(rng, (T, d), 1.0))
 
 
+# ---- device-side draws for the 16-layer stack (12.9 GB of weights: host draws would take
+# minutes).  torch's seeded Philox generator on the GPU, fp32 normal draws scaled in fp32,
+# bf16 by round-to-nearest-even; the same (seed, stream) gives the same tensor on the same
+# torch build.  Both the GPU run and the oracle read these tensors (the oracle a host copy).
+
+def device_normal_bf16(shape, stream: int, std: float, seed: int = 0, device="cuda"):
+    import torch
+    g = torch.Generator(device=device)
+    g.manual_seed(seed * 1_000_003 + stream)
+    a = torch.randn(tuple(shape), generator=g, device=device, dtype=torch.float32) * std
+    return a.to(torch.bfloat16)
+
+
+def device_stack_layer(l: int, d: int = 2048, N: int = 64, m: int = 1024, seed: int = 0,
+                       device="cuda"):
+    """(W_router [N, d], W_gate_up [N, 2m, d], W_down [N, d, m]) of stack layer l, bf16 on
+    the device, weights ~ N(0, 0.02)."""
+    import torch
+    base = 16 * (l + 1)
+    Wr = device_normal_bf16((N, d), base + 1, 0.02, seed, device)
+    Wgu = torch.cat([device_normal_bf16((N, m, d), base + 2, 0.02, seed, device),
+                     device_normal_bf16((N, m, d), base + 3, 0.02, seed, device)], dim=1)
+    Wd = device_normal_bf16((N, d, m), base + 4, 0.02, seed, device)
+    return Wr, Wgu, Wd
+
+
+def device_stack_input(T: int = 16384, d: int = 2048, seed: int = 0, device="cuda"):
+    """x [T, d] ~ N(0, 1), bf16 on the device."""
+    return device_normal_bf16((T, d), 0, 1.0, seed, device)
+
+
 def planted_logits(T: int = 65536, N: int = 64, seed=0, m_max: int = 8,
                    delta_lo: float = 2.0, delta_hi: float = 6.0) -> np.ndarray:
     """Routing-only workload: fp32 logits [T, N].
