@@ -68,7 +68,7 @@ def time_layer(B, torch, args_gpu, K, mode, steps, warmup, profile, packed=None)
     return dt / steps * 1e3, {n: ms / cnt for n, (ms, cnt) in kern.items()}
 
 
-def routing_only(B, torch, T=65536, N=64, K=8, nbuf=32, iters=64):
+def routing_only(B, torch, T=65536, N=64, K=8, nbuf=32, iters=64, big_T=0):
     """Routing kernel alone on the routing-only workload (planted logits), rotating over
     nbuf distinct logit buffers (nbuf * 16.8 MB > the 256 MB last-level cache)."""
     from paper_2608_04401_amd import synth
@@ -101,6 +101,33 @@ def routing_only(B, torch, T=65536, N=64, K=8, nbuf=32, iters=64):
     out = {"workload": "routing-only T=%d N=%d K=%d planted logits" % (T, N, K),
            "kernel": "route", "us": round(us, 3), "bytes": nbytes, "GB/s": round(gbs, 1),
            "peak": PEAK_HBM_GBS, "frac": round(gbs / PEAK_HBM_GBS, 4)}
+    if big_T:
+        # supplementary point: the same kernel on 2^20 tokens (16 waves per SIMD), two
+        # 268 MB logit buffers in turn (more than the last-level cache)
+        lg2 = torch.from_numpy(synth.planted_logits(big_T, N, seed=1)).cuda()
+        bufs2 = [lg2, lg2.clone()]
+        k2 = torch.empty(big_T, dtype=torch.int32, device="cuda")
+        ids2 = torch.empty((big_T, K), dtype=torch.int32, device="cuda")
+        w2 = torch.empty((big_T, K), dtype=torch.float32, device="cuda")
+        call = lambda b: L.elb_route(C.c_void_p(b.data_ptr()), big_T, N, C.byref(p),
+                                     C.c_void_p(k2.data_ptr()), C.c_void_p(ids2.data_ptr()),
+                                     C.c_void_p(w2.data_ptr()), st)
+        for i in range(4):
+            call(bufs2[i % 2])
+        torch.cuda.synchronize()
+        B.elb_profile_read()
+        B.elb_profile_enable(True)
+        for i in range(16):
+            call(bufs2[i % 2])
+        torch.cuda.synchronize()
+        B.elb_profile_enable(False)
+        ms2, cnt2 = B.elb_profile_read()["route"]
+        us2 = ms2 / cnt2 * 1e3
+        nb2 = big_T * N * 4 + big_T * (4 + 8 * K)
+        out["T_2^20"] = {"us": round(us2, 2), "bytes": nb2,
+                         "GB/s": round(nb2 / (us2 * 1e-6) / 1e9, 1),
+                         "frac": round(nb2 / (us2 * 1e-6) / 1e9 / PEAK_HBM_GBS, 4)}
+        del lg2, bufs2, k2, ids2, w2
     # variable-k dispatch of that routing (histogram, scan, scatter)
     for _ in range(4):
         B.elb_dispatch(k, ids, N)
@@ -445,7 +472,7 @@ def main():
                            stats.load_balance_report(counts, counts_top, K, T).items()}
     if not args.no_routing:
         log("routing-only kernel")
-        res["routing_kernel"] = routing_only(B, torch)
+        res["routing_kernel"] = routing_only(B, torch, big_T=1 << 20)
         log("routing variants")
         res["routing_variants"] = routing_variants(B, torch)
     if args.workload == "olmoe-prefill" and not args.no_decode:
