@@ -413,7 +413,9 @@ static int moe_forward_entry(const void* x, const void* W_router, const void* W_
     int* k = k_out ? k_out : (int*)(ws + L.k);
     int* ids = ids_out ? ids_out : (int*)(ws + L.ids);
     float* w = w_out ? w_out : (float*)(ws + L.w);
-    if (router_route_fusable(dtype, K)) {
+    // small batches with N = 64: the expert-split router and the 16-lane routing (two short
+    // launches) beat the fused kernel, whose blocks each read all of W_r; same bits either way
+    if (router_route_fusable(dtype, K) && !(N == 64 && T <= kSmallBatch)) {
         if (int rc = hip_status(launch_router_route(x, W_router, T, d, N, *params, logits_out,
                                                     k, ids, w, s), "router_route"))
             return rc;

@@ -43,6 +43,9 @@ hipError_t launch_route(const float* logits, int64_t T, int N, const elb_route_p
 // routing variants (caps above kLaneMaxK, tail randomisation when `rand` is set, the elbow
 // index `e` and angle `theta` when set); ids == nullptr: no selection (diagnostics only)
 constexpr int kLaneMaxK = 16;  // largest cap of the lane-per-token routing kernel
+// batches of at most this many tokens are latency-bound: the router GEMM splits the experts
+// over blocks and the routing gives each token 16 lanes (N = 64)
+constexpr int64_t kSmallBatch = 1024;
 hipError_t launch_route_pair(const float* logits, const float* rand, int64_t T, int N,
                              const elb_route_params& p, int* k, int* ids, float* w, int* e,
                              float* theta, hipStream_t s);

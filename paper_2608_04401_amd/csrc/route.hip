@@ -218,9 +218,40 @@ hipError_t launch_np(const float* logits, int64_t T, int N, const elb_route_para
     return hipGetLastError();
 }
 
+// ---- route_x16_kernel: small batches with N = 64, 16 lanes per token (route_token_x16),
+// 16 tokens per block ----
+template <int KMAX>
+__global__ __launch_bounds__(256) void route_x16_kernel(const float* __restrict__ logits,
+                                                        int64_t T, int K, float eps, int mode,
+                                                        int renorm, XTable xt,
+                                                        int* __restrict__ kout,
+                                                        int* __restrict__ ids,
+                                                        float* __restrict__ wout) {
+    __shared__ float rows[16][65];
+    const int64_t t0 = (int64_t)blockIdx.x * 16;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        const int i = threadIdx.x + 256 * q;
+        const int r = i >> 6, c = i & 63;
+        const int64_t t = t0 + r;
+        rows[r][c] = (t < T) ? logits[t * 64 + c] : 0.f;  // rows past T: finite, never stored
+    }
+    __syncthreads();
+    const int tr = threadIdx.x >> 4;
+    route_token_x16<KMAX>(&rows[tr][0], K, eps, mode, renorm, xt, t0 + tr, t0 + tr < T, kout,
+                          ids, wout);
+}
+
 template <int KMAX>
 hipError_t launch_k(const float* logits, int64_t T, int N, const elb_route_params& p, int* k,
                    int* ids, float* w, hipStream_t s) {
+    if (N == 64 && T <= kSmallBatch) {
+        ProfileScope prof("route", s);
+        hipLaunchKernelGGL((route_x16_kernel<KMAX>), dim3((unsigned)((T + 15) / 16)), dim3(256),
+                           0, s, logits, T, p.K, p.eps, p.mode, p.renormalize, make_xtable(N), k,
+                           ids, w);
+        return hipGetLastError();
+    }
     switch (N) {
         case 8: return launch_np<8, true, KMAX>(logits, T, N, p, k, ids, w, s);
         case 16: return launch_np<16, true, KMAX>(logits, T, N, p, k, ids, w, s);

@@ -16,11 +16,14 @@ namespace {
 
 constexpr int RW = 4;  // waves per router block
 
-// The 16 x N logits of tokens [t0, t0 + 16): each wave's partial sums over its k-steps go to
-// part[w] (lane rows, expert columns); the caller sums the RW partial tiles.
+// The logits of tokens [t0, t0 + 16) and experts [16 g0, 16 (g0 + NG)) (NG groups of 16):
+// each wave's partial sums over its k-steps go to part[w] (lane rows, expert columns
+// 16 g + ..., g < NG); the caller sums the RW partial tiles.  Every logit is computed the same
+// way whatever NG and g0 are (its own MFMA column, the same k-steps per wave, the same sum).
+template <int NG>
 __device__ __forceinline__ void router_partials(const bf16_t* __restrict__ x,
                                                 const bf16_t* __restrict__ Wr, int64_t T,
-                                                int d, int N, int64_t t0,
+                                                int d, int N, int64_t t0, int g0,
                                                 float (&part)[RW][16][65]) {
     const int lane = threadIdx.x & 63;
     const int w = threadIdx.x >> 6;
@@ -29,15 +32,15 @@ __device__ __forceinline__ void router_partials(const bf16_t* __restrict__ x,
     const int64_t ta = t0 + l16;
     const bool arow = ta < T;
     const bf16_t* ap = x + (arow ? ta : 0) * d + kq;
-    const bf16_t* bp[4];
+    const bf16_t* bp[NG];
 #pragma unroll
-    for (int g = 0; g < 4; ++g) {
-        const int n = 16 * g + l16;
+    for (int g = 0; g < NG; ++g) {
+        const int n = 16 * (g0 + g) + l16;
         bp[g] = Wr + (int64_t)(n < N ? n : 0) * d + kq;
     }
-    f32x4_t acc[4];
+    f32x4_t acc[NG];
 #pragma unroll
-    for (int g = 0; g < 4; ++g) acc[g] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    for (int g = 0; g < NG; ++g) acc[g] = f32x4_t{0.f, 0.f, 0.f, 0.f};
     // wave w takes the 32-deep k-steps w, w + RW, w + 2 RW, ... (its steps j = 0, 1, ...).  A
     // ring of R register slots keeps R - 1 steps in flight: step j lives in slot j % R, and
     // while step j is multiplied, step j + R - 1 is loaded into the slot step j - 1 has just
@@ -45,17 +48,17 @@ __device__ __forceinline__ void router_partials(const bf16_t* __restrict__ x,
     constexpr int R = 5;
     const int nsteps = d / 32;
     const int mine = (nsteps - w + RW - 1) / RW;  // steps of this wave
-    bf16x8_t ra[R], rb[R][4];
-    auto load = [&](int slot_j, bf16x8_t& a, bf16x8_t (&bb)[4]) {
+    bf16x8_t ra[R], rb[R][NG];
+    auto load = [&](int slot_j, bf16x8_t& a, bf16x8_t (&bb)[NG]) {
         const int k0 = (slot_j < mine ? w + RW * slot_j : 0) * 32;  // past the end: step 0
         a = *reinterpret_cast<const bf16x8_t*>(ap + k0);
 #pragma unroll
-        for (int g = 0; g < 4; ++g) bb[g] = *reinterpret_cast<const bf16x8_t*>(bp[g] + k0);
+        for (int g = 0; g < NG; ++g) bb[g] = *reinterpret_cast<const bf16x8_t*>(bp[g] + k0);
     };
     // rows past T and experts past N read row 0 and give logits that are never written
-    auto mma = [&](const bf16x8_t& a, const bf16x8_t (&bb)[4]) {
+    auto mma = [&](const bf16x8_t& a, const bf16x8_t (&bb)[NG]) {
 #pragma unroll
-        for (int g = 0; g < 4; ++g)
+        for (int g = 0; g < NG; ++g)
             acc[g] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, bb[g], acc[g], 0, 0, 0);
     };
 #pragma unroll
@@ -79,7 +82,7 @@ __device__ __forceinline__ void router_partials(const bf16_t* __restrict__ x,
     }
     const int rq = (lane >> 4) * 4;
 #pragma unroll
-    for (int g = 0; g < 4; ++g)
+    for (int g = 0; g < NG; ++g)
 #pragma unroll
         for (int r = 0; r < 4; ++r) part[w][rq + r][16 * g + l16] = acc[g][r];
 }
@@ -93,19 +96,25 @@ __device__ __forceinline__ float router_sum(const float (&part)[RW][16][65], int
     return v;
 }
 
+// NG = 4: a block computes all N <= 64 experts of its 16 tokens; NG = 1 (few tokens): one
+// block per (16 tokens, 16 experts) — blockIdx.y is the expert group — so the reads of W_r
+// are spread over N / 16 times more compute units
+template <int NG>
 __global__ __launch_bounds__(64 * RW) void router_bf16(const bf16_t* __restrict__ x,
                                                       const bf16_t* __restrict__ Wr, int64_t T,
                                                       int d, int N, float* __restrict__ logits) {
     __shared__ float part[RW][16][65];  // per-wave partial logits (padded rows)
     const int64_t t0 = (int64_t)blockIdx.x * 16;
-    router_partials(x, Wr, T, d, N, t0, part);
+    const int g0 = (NG == 4) ? 0 : (int)blockIdx.y;
+    router_partials<NG>(x, Wr, T, d, N, t0, g0, part);
     __syncthreads();
 #pragma unroll
-    for (int q = 0; q < 1024 / (64 * RW); ++q) {
+    for (int q = 0; q < 256 * NG / (64 * RW); ++q) {
         const int o = threadIdx.x + 64 * RW * q;
-        const int tr = o >> 6, n = o & 63;
+        const int tr = o / (16 * NG), nl = o % (16 * NG);
         const int64_t t = t0 + tr;
-        if (t < T && n < N) logits[t * N + n] = router_sum(part, tr, n);
+        const int n = 16 * g0 + nl;
+        if (t < T && n < N) logits[t * N + n] = router_sum(part, tr, nl);
     }
 }
 
@@ -121,7 +130,7 @@ __global__ __launch_bounds__(64 * RW) void router_route_bf16(
     int* __restrict__ kout, int* __restrict__ ids, float* __restrict__ wout) {
     __shared__ float part[RW][16][65];
     const int64_t t0 = (int64_t)blockIdx.x * 16;
-    router_partials(x, Wr, T, d, N, t0, part);
+    router_partials<4>(x, Wr, T, d, N, t0, 0, part);
     __syncthreads();
 #pragma unroll
     for (int q = 0; q < 1024 / (64 * RW); ++q) {
@@ -204,8 +213,13 @@ hipError_t launch_router(const void* x, const void* Wr, int64_t T, int d, int N,
     if (T == 0) return hipSuccess;
     if (dtype == ELB_BF16) {
         ProfileScope prof("router_bf16", s);
-        hipLaunchKernelGGL(router_bf16, dim3((unsigned)((T + 15) / 16)), dim3(64 * RW), 0, s,
-                           (const bf16_t*)x, (const bf16_t*)Wr, T, d, N, logits);
+        if (T <= kSmallBatch)
+            hipLaunchKernelGGL(router_bf16<1>, dim3((unsigned)((T + 15) / 16), (unsigned)((N + 15) / 16)),
+                               dim3(64 * RW), 0, s, (const bf16_t*)x, (const bf16_t*)Wr, T, d,
+                               N, logits);
+        else
+            hipLaunchKernelGGL(router_bf16<4>, dim3((unsigned)((T + 15) / 16)), dim3(64 * RW), 0,
+                               s, (const bf16_t*)x, (const bf16_t*)Wr, T, d, N, logits);
     } else {
         ProfileScope prof("router_f32", s);
         hipLaunchKernelGGL(router_f32, dim3((unsigned)((T * N + 255) / 256)), dim3(256), 0, s,
