@@ -9,11 +9,18 @@
 // M-tiles [tile_off[e], tile_off[e+1]); both come from the dispatch scan, on the device, so
 // the grid is launched with an upper bound of M-tiles and surplus blocks exit at once.
 //
-// bf16 path: CDNA4 MFMA v_mfma_f32_16x16x32_bf16, fp32 accumulation, block tile 128 x 128 x 64,
-// 4 waves (2 x 2), 64 x 64 per wave, LDS double buffered with register prefetch, rows padded
-// by 8 bf16 so that 16 lanes reading 16-byte fragments of 16 consecutive rows hit distinct
-// banks.  In gate_up the 128 B-tile columns are 64 gate and the matching 64 up columns, and
-// each wave owns matching gate/up 16-column pairs, so SwiGLU is applied in registers.
+// Kernels (all fp32 accumulation; the launchers at the end pick one per problem):
+//  - gemm_bf16_dma: the prefill kernel (on average at least 192 rows per expert).  Block tile
+//    256 x 256 x 64, 4 waves of 128 x 128 on v_mfma_f32_32x32x16_bf16, operands copied
+//    global -> LDS by global_load_lds_dwordx4 into a 5-unit ring; remainder rows of a few
+//    experts (TilePlan) go to extra blocks of the same launch (weight-streaming tasks of
+//    gemm_stream.h).  Described in detail above the kernel.
+//  - gemm_bf16: smaller problems.  v_mfma_f32_16x16x32_bf16, block tile 128 x 128 x 64,
+//    4 waves (2 x 2) of 64 x 64, LDS double buffered with register prefetch, rows padded by
+//    8 bf16 so that 16 lanes reading 16-byte fragments of 16 consecutive rows hit distinct
+//    banks.  In gate_up the 128 B-tile columns are 64 gate and the matching 64 up columns,
+//    and each wave owns matching gate/up 16-column pairs, so SwiGLU is applied in registers.
+//  - decode-sized batches use gemm_skinny.hip instead (weight streaming).
 // fp32 path: plain VALU FMA tiles (64 x 64 x 16), for the fp32 configuration.
 #include "gemm_stream.h"
 

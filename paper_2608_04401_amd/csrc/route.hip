@@ -13,6 +13,9 @@
 //    16-byte stores.
 //  - route_kernel (any N <= 64): the rows staged through registers into a padded LDS tile;
 //    every lane routes its token from its row and stores its own outputs.
+//  - route_x16_kernel (N = 64, batches of at most kSmallBatch tokens): 16 lanes per token
+//    (route_token_x16: a bitonic sort across the 16 lanes), 16 tokens per block, so that a
+//    small batch still spreads over many compute units.  The same bits as the other two.
 #include "route_lane.h"
 
 namespace elb {
