@@ -230,6 +230,51 @@ def decode_layer(B, torch, synth, K=8, steps=100):
     return out
 
 
+def stack_16_layers(B, torch, synth, K=8, passes=3, T=16384, d=2048, N=64, m=1024, layers=16):
+    """Sixteen stacked OLMoE-shaped layers with a residual add between them (h <- h + MoE_l(h)),
+    T tokens, elbow routing and top-K on the same inputs: end-to-end tokens/s, mean k and the
+    per-expert load CV of every layer.  Weights are drawn on the device, N(0, 0.02), one seeded
+    stream per tensor (the inputs of the 16-layer GPU parity test)."""
+    from paper_2608_04401_amd import stats
+    W = [synth.device_stack_layer(l, d, N, m) for l in range(layers)]
+    x0 = synth.device_stack_input(T, d)
+    out = {"workload": "%d stacked layers: T=%d d_model=%d N=%d m=%d K=%d bf16, residual add "
+                       "between layers" % (layers, T, d, N, m, K)}
+
+    def run(mode, debug=False):
+        h, ks, cvs = x0, [], []
+        for Wr, Wgu, Wd in W:
+            if debug:
+                h, dbg = B.elb_moe_forward(h, Wr, Wgu, Wd, K=K, mode=mode, residual=h, debug=True)
+                c = dbg["counts"].cpu().numpy()
+                ks.append(float(c.sum()) / T)
+                cvs.append(stats.cv(stats.utilization(c)))
+            else:
+                h = B.elb_moe_forward(h, Wr, Wgu, Wd, K=K, mode=mode, residual=h)
+        return ks, cvs
+
+    for name, mode in (("elbow", B.MODE_ELBOW), ("topk", B.MODE_TOPK)):
+        ks, cvs = run(mode, debug=True)
+        run(mode)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(passes):
+            run(mode)
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / passes
+        out[name] = {"tokens_per_s": round(T / (ms * 1e-3), 1), "ms_per_pass": round(ms, 3),
+                     "mean_k": round(sum(ks) / len(ks), 4),
+                     "mean_k_per_layer": [round(v, 3) for v in ks],
+                     "load_cv_per_layer": [round(v, 4) for v in cvs]}
+    out["elbow_vs_topk_latency_change_pct"] = round(
+        (out["elbow"]["ms_per_pass"] - out["topk"]["ms_per_pass"]) / out["topk"]["ms_per_pass"]
+        * 100, 2)
+    del W
+    return out
+
+
 def dispatch_bytes(T, N, K, sum_k):
     """Algorithmic bytes of the dispatch: reads k [T] and ids [T, K]; writes counts [N],
     offsets [N + 1], row_token [sum k] and inv [T, K] (int32)."""
@@ -320,6 +365,7 @@ def main():
     ap.add_argument("--no-routing", action="store_true")
     ap.add_argument("--no-topk", action="store_true", help="skip the fixed top-K baseline")
     ap.add_argument("--no-decode", action="store_true", help="skip the decode-sized layer")
+    ap.add_argument("--no-stack", action="store_true", help="skip the 16-layer stack")
     ap.add_argument("--counters", action="store_true",
                     help="run only the workload of the HBM-traffic counter runs")
     ap.add_argument("--routing-counters", action="store_true",
@@ -478,6 +524,9 @@ def main():
     if args.workload == "olmoe-prefill" and not args.no_decode:
         log("decode-sized layer")
         res["decode_layer"] = decode_layer(B, torch, synth)
+    if args.workload == "olmoe-prefill" and not args.no_stack:
+        log("16-layer stack")
+        res["stack_16_layers"] = stack_16_layers(B, torch, synth)
     if not args.no_cpu_baseline:
         log("cpu baseline (oracle)")
         res["cpu_baseline"] = cpu_baseline(L, K)
