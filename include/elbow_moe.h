@@ -12,7 +12,8 @@
  * Conventions for every entry point:
  *  - All tensor pointers are DEVICE pointers owned by the caller; row-major, densely packed.
  *    The library never allocates, frees or synchronises device memory; scratch space
- *    comes only from the caller's workspace.  Nothing is retained between calls.
+ *    comes only from the caller's workspace, which must be 256-byte aligned (as hipMalloc
+ *    and torch allocations are).  Nothing is retained between calls.
  *  - `stream` is a hipStream_t passed as void* (NULL = the null stream).  Kernels are
  *    enqueued on it and the call returns without waiting for them.
  *  - Arguments are validated on the host BEFORE anything is enqueued.  On any error
@@ -48,7 +49,8 @@ typedef enum {
     ELB_OK = 0,
     ELB_ERR_INVALID_ARG = 1, /* null pointer, negative size, K outside [1, N], eps < 0, ... */
     ELB_ERR_UNSUPPORTED = 2, /* a size outside what the kernels implement (e.g. N > 64) */
-    ELB_ERR_WORKSPACE = 3,   /* workspace missing or smaller than elb_*_workspace_bytes */
+    ELB_ERR_WORKSPACE = 3,   /* workspace missing, not 256-byte aligned or smaller than
+                                elb_*_workspace_bytes */
     ELB_ERR_HIP = 4          /* a HIP launch error (hipGetLastError after the launch) */
 } elb_status;
 

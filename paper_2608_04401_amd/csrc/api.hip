@@ -53,7 +53,7 @@ Layout layout(int64_t T, int d, int N, int m, int K, int dtype) {
         return at;
     };
     const size_t rows = (size_t)T * K;
-    L.hist = take((size_t)dispatch_groups(T) * N * 4);
+    L.hist = take((size_t)dispatch_hist_ints(T, N) * 4);
     L.tile_off = take((size_t)(N + 1 + kTailMax + 1) * 4);  // tile_off, then tail_list
     L.counts = take((size_t)N * 4);
     L.offsets = take((size_t)(N + 1) * 4);
@@ -269,7 +269,7 @@ int elb_elbow_angle(const float* logits, int64_t T, int32_t N, float eps, int32_
 
 size_t elb_dispatch_workspace_bytes(int64_t T, int32_t N) {
     if (T < 0 || N < 1) return 0;
-    return align_up((size_t)dispatch_groups(T) * N * 4) +
+    return align_up((size_t)dispatch_hist_ints(T, N) * 4) +
            align_up((size_t)(N + 1 + kTailMax + 1) * 4);
 }
 
@@ -289,9 +289,11 @@ int elb_dispatch(const int32_t* k, const int32_t* ids, int64_t T, int32_t N, int
     const size_t need = elb_dispatch_workspace_bytes(T, N);
     if (!workspace || workspace_bytes < need)
         return fail(ELB_ERR_WORKSPACE, "workspace of %zu bytes, need %zu", workspace_bytes, need);
+    if ((uintptr_t)workspace % kAlign)
+        return fail(ELB_ERR_WORKSPACE, "workspace not %zu-byte aligned", kAlign);
     char* ws = (char*)workspace;
     int* hist = (int*)ws;
-    int* tile_off = (int*)(ws + align_up((size_t)dispatch_groups(T) * N * 4));
+    int* tile_off = (int*)(ws + align_up((size_t)dispatch_hist_ints(T, N) * 4));
     const TilePlan plan{128, 0, 1, kTailMax};  // plain ceil(c / 128) tiles, no tail list use
     return hip_status(launch_dispatch(k, ids, T, N, K, counts, offsets, row_token, inv, hist,
                                       tile_off, tile_off + N + 1, plan, (hipStream_t)stream),
@@ -369,6 +371,8 @@ static int moe_experts_entry(const void* x, const void* W_gate_up, const void* W
     if (!workspace || workspace_bytes < L.experts_end)
         return fail(ELB_ERR_WORKSPACE, "workspace of %zu bytes, need %zu", workspace_bytes,
                     L.experts_end);
+    if ((uintptr_t)workspace % kAlign)
+        return fail(ELB_ERR_WORKSPACE, "workspace not %zu-byte aligned", kAlign);
     return experts_impl(x, W_gate_up, W_down, packed, k, ids, w, residual, T, d, N, m, K, dtype, y,
                         (char*)workspace, L, nullptr, (hipStream_t)stream);
 }
@@ -407,6 +411,8 @@ static int moe_forward_entry(const void* x, const void* W_router, const void* W_
     if (!workspace || workspace_bytes < L.total)
         return fail(ELB_ERR_WORKSPACE, "workspace of %zu bytes, need %zu", workspace_bytes,
                     L.total);
+    if ((uintptr_t)workspace % kAlign)
+        return fail(ELB_ERR_WORKSPACE, "workspace not %zu-byte aligned", kAlign);
     char* ws = (char*)workspace;
     hipStream_t s = (hipStream_t)stream;
     float* logits = logits_out ? logits_out : (float*)(ws + L.logits);

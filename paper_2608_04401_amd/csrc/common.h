@@ -50,8 +50,11 @@ hipError_t launch_route_pair(const float* logits, const float* rand, int64_t T, 
                              const elb_route_params& p, int* k, int* ids, float* w, int* e,
                              float* theta, hipStream_t s);
 
-// dispatch: number of 64-token groups and the workspace it needs
+// dispatch: number of 64-token groups; the histogram's row stride (groups rounded up to a
+// multiple of 4, so that every expert's row is 16-byte aligned) and its size in ints
 inline int64_t dispatch_groups(int64_t T) { return (T + kWave - 1) / kWave; }
+inline int64_t dispatch_hist_ld(int64_t T) { return (dispatch_groups(T) + 3) & ~(int64_t)3; }
+inline int64_t dispatch_hist_ints(int64_t T, int N) { return dispatch_hist_ld(T) * N; }
 
 // M-tiling of the grouped GEMMs, computed by the dispatch on the device from the counts.
 // Each expert gets ceil(c / tile_rows) M-tiles, except that with tail_rows > 0 an expert with
@@ -67,7 +70,8 @@ struct TilePlan {
 constexpr int kTailMax = 16;   // most experts whose remainders go to the tail kernel
 constexpr int kTailRows = 32;  // largest remainder the tail kernel takes
 
-// hist [groups, N] int32 scratch; tile_off [N + 1]; tail_list [kTailMax + 1]
+// hist: dispatch_hist_ints(T, N) int32 scratch ([N, dispatch_hist_ld(T)], expert-major);
+// tile_off [N + 1]; tail_list [kTailMax + 1]
 hipError_t launch_dispatch(const int* k, const int* ids, int64_t T, int N, int K, int* counts,
                            int* offsets, int* row_token, int* inv, int* hist, int* tile_off,
                            int* tail_list, const TilePlan& plan, hipStream_t s);

@@ -1,9 +1,10 @@
 // Variable-k dispatch: per-expert token lists from a routing (k_t experts per token).
 //
-// Three launches (one for T <= 256, dispatch_small below), deterministic, no atomics:
+// Deterministic, no atomics.  Three launches for large batches:
 //   count   one lane per token; a wave ORs each token's selected experts into a 64-bit mask
 //           and, per expert, counts the wave's tokens with one ballot + popcount.  The
-//           per-wave counts form an expert-major [N, groups] histogram.
+//           per-wave counts form an expert-major [N, groups] histogram (row stride ld, a
+//           multiple of 4).
 //   scan    one block per expert: an exclusive prefix over groups (the base of each group
 //           inside the expert's list) and the expert's total.
 //   scatter one lane per token again.  Each wave first forms the exclusive prefix of the
@@ -12,12 +13,19 @@
 //           e is the popcount of the expert's ballot below the lane, and its row is
 //           offsets[e] + base[e, group] + rank.  Rows within an expert are therefore in
 //           increasing token order.
+// Up to kDirectGroups groups (T <= 8192) the scan launch is skipped: every scatter wave reads
+// its experts' whole histogram rows (lane e: row e, 16-byte loads all in flight at once) and
+// forms the expert totals and its own group's base itself.  One launch (dispatch_small) for
+// T <= 256.  All three forms give the same rows.
 // Requires N <= 64 (one mask bit per expert).
 #include "common.h"
 
 namespace elb {
 
 namespace {
+
+// waves (64-token groups) per block of the count and scatter kernels
+constexpr int kDispWaves = 1;
 
 // slots j0 .. j0 + 7 of token t's ids (-1 past K): eight independent loads, so a lane waits
 // for memory once per eight slots rather than once per slot
@@ -77,11 +85,11 @@ __device__ __forceinline__ void write_tail_list(bool tail_mine, int n_tail, int 
     if (lane == 0) tail_list[0] = n_tail;
 }
 
-__global__ __launch_bounds__(256) void dispatch_count(const int* __restrict__ k,
-                                                      const int* __restrict__ ids, int64_t T,
-                                                      int N, int K, int* __restrict__ hist) {
+__global__ __launch_bounds__(64 * kDispWaves) void dispatch_count(
+    const int* __restrict__ k, const int* __restrict__ ids, int64_t T, int N, int K, int64_t ld,
+    int* __restrict__ hist) {
     const int lane = threadIdx.x & (kWave - 1);
-    const int64_t g = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    const int64_t g = (int64_t)blockIdx.x * kDispWaves + (threadIdx.x >> 6);
     const int64_t t = g * kWave + lane;
     const int64_t groups = (T + kWave - 1) / kWave;
     if (g >= groups) return;  // wave-uniform
@@ -92,18 +100,18 @@ __global__ __launch_bounds__(256) void dispatch_count(const int* __restrict__ k,
         const int c = __popcll(b);
         if (lane == e) mine = c;
     }
-    if (lane < N) hist[(int64_t)lane * groups + g] = mine;
+    if (lane < N) hist[(int64_t)lane * ld + g] = mine;
 }
 
 // one block per expert e: exclusive prefix of hist[e, :] over the groups, in place
 __global__ __launch_bounds__(1024) void dispatch_scan(int* __restrict__ hist, int64_t groups,
-                                                     int* __restrict__ counts) {
+                                                     int64_t ld, int* __restrict__ counts) {
     __shared__ int wsum[16];
     const int e = blockIdx.x;
     const int tid = threadIdx.x;
     const int lane = tid & (kWave - 1);
     const int wv = tid >> 6;
-    int* h = hist + (int64_t)e * groups;
+    int* h = hist + (int64_t)e * ld;
     const int64_t chunk = (groups + 1023) / 1024;  // consecutive groups per thread
     const int64_t g0 = tid * chunk;
     const int64_t g1 = (g0 + chunk < groups) ? g0 + chunk : groups;
@@ -132,28 +140,54 @@ __global__ __launch_bounds__(1024) void dispatch_scan(int* __restrict__ hist, in
     if (tid == 0) counts[e] = total;
 }
 
-__global__ __launch_bounds__(256) void dispatch_scatter(const int* __restrict__ k,
-                                                        const int* __restrict__ ids, int64_t T,
-                                                        int N, int K,
-                                                        const int* __restrict__ hist,
-                                                        const int* __restrict__ counts,
-                                                        int* __restrict__ offsets,
-                                                        int* __restrict__ tile_off,
-                                                        int* __restrict__ tail_list,
-                                                        TilePlan plan,
-                                                        int* __restrict__ row_token,
-                                                        int* __restrict__ inv) {
-    __shared__ int pos[4][kWave][kWave + 1];
+constexpr int kDirectGroups = 128;  // most groups whose histogram the scatter sums itself
+
+// DIRECT: hist holds the raw per-group counts (no scan launch) and counts is written here
+template <bool DIRECT>
+__global__ __launch_bounds__(64 * kDispWaves) void dispatch_scatter(
+    const int* __restrict__ k, const int* __restrict__ ids, int64_t T, int N, int K, int64_t ld,
+    const int* __restrict__ hist, int* __restrict__ counts, int* __restrict__ offsets,
+    int* __restrict__ tile_off, int* __restrict__ tail_list, TilePlan plan,
+    int* __restrict__ row_token, int* __restrict__ inv) {
+    __shared__ int pos[kDispWaves][kWave][kWave + 1];
     const int lane = threadIdx.x & (kWave - 1);
     const int wv = threadIdx.x >> 6;
-    const int64_t g = (int64_t)blockIdx.x * 4 + wv;
+    const int64_t g = (int64_t)blockIdx.x * kDispWaves + wv;
     const int64_t t = g * kWave + lane;
     const int64_t groups = (T + kWave - 1) / kWave;
     // expert list offsets and M-tile offsets: exclusive prefixes over the experts (lane e).
-    // The group's histogram entry is loaded together with the totals (one memory round trip
-    // for both; surplus waves read group 0's, unused).
-    const int c = (lane < N) ? counts[lane] : 0;
-    const int hist_mine = (lane < N) ? hist[(int64_t)lane * groups + (g < groups ? g : 0)] : 0;
+    // c: expert e's total; hist_mine: the base of this group inside expert e's list.
+    int c = 0, hist_mine = 0;
+    if (DIRECT) {
+        // lane e sums row e of the raw histogram: all of it (the total) and the groups below
+        // g (the base), in group order; pads past `groups` are not read as counts
+        if (lane < N) {
+            const int4* h4 = reinterpret_cast<const int4*>(hist + (int64_t)lane * ld);
+            const int n4 = (int)(ld >> 2), ng = (int)groups, gg = (int)g;
+            int4 v[kDirectGroups / 4];
+#pragma unroll
+            for (int q = 0; q < kDirectGroups / 4; ++q) {
+                v[q] = make_int4(0, 0, 0, 0);
+                if (q < n4) v[q] = h4[q];
+            }
+#pragma unroll
+            for (int q = 0; q < kDirectGroups / 4; ++q) {
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const int gi = 4 * q + r;
+                    const int x0 = r == 0 ? v[q].x : r == 1 ? v[q].y : r == 2 ? v[q].z : v[q].w;
+                    const int x = gi < ng ? x0 : 0;
+                    c += x;
+                    hist_mine += gi < gg ? x : 0;
+                }
+            }
+        }
+    } else {
+        // the group's (scanned) histogram entry is loaded together with the totals (one
+        // memory round trip for both; surplus waves read group 0's, unused)
+        c = (lane < N) ? counts[lane] : 0;
+        hist_mine = (lane < N) ? hist[(int64_t)lane * ld + (g < groups ? g : 0)] : 0;
+    }
     bool tail_mine;
     int n_tail;
     const int tiles = plan_tiles(c, lane, N, plan, tail_mine, n_tail);  // whole wave
@@ -171,6 +205,7 @@ __global__ __launch_bounds__(256) void dispatch_scatter(const int* __restrict__ 
         if (lane < N) {
             offsets[lane] = off_mine;
             tile_off[lane] = tincl - tiles;
+            if (DIRECT) counts[lane] = c;
         }
         if (lane == N - 1) {
             offsets[N] = incl;
@@ -313,23 +348,32 @@ hipError_t launch_dispatch(const int* k, const int* ids, int64_t T, int N, int K
         return hipGetLastError();
     }
     const int64_t groups = dispatch_groups(T);
+    const int64_t ld = dispatch_hist_ld(T);
+    const bool direct = groups <= kDirectGroups;
     // at least one scatter block, which also writes offsets and tile_off (also when T == 0)
-    const unsigned blocks = (unsigned)((groups + 3) / 4 > 0 ? (groups + 3) / 4 : 1);
+    const int64_t nb = (groups + kDispWaves - 1) / kDispWaves;
+    const unsigned blocks = (unsigned)(nb > 0 ? nb : 1);
     {
         ProfileScope prof("dispatch_count", s);
         if (T > 0)
-            hipLaunchKernelGGL(dispatch_count, dim3(blocks), dim3(256), 0, s, k, ids, T, N, K,
-                               hist);
+            hipLaunchKernelGGL(dispatch_count, dim3(blocks), dim3(64 * kDispWaves), 0, s, k,
+                               ids, T, N, K, ld, hist);
     }
-    {
+    if (!direct) {
         ProfileScope prof("dispatch_scan", s);
-        hipLaunchKernelGGL(dispatch_scan, dim3((unsigned)N), dim3(1024), 0, s, hist, groups,
+        hipLaunchKernelGGL(dispatch_scan, dim3((unsigned)N), dim3(1024), 0, s, hist, groups, ld,
                            counts);
     }
     {
         ProfileScope prof("dispatch_scatter", s);
-        hipLaunchKernelGGL(dispatch_scatter, dim3(blocks), dim3(256), 0, s, k, ids, T, N, K,
-                           hist, counts, offsets, tile_off, tail_list, plan, row_token, inv);
+        if (direct)
+            hipLaunchKernelGGL(dispatch_scatter<true>, dim3(blocks), dim3(64 * kDispWaves), 0,
+                               s, k, ids, T, N, K, ld, hist, counts, offsets, tile_off,
+                               tail_list, plan, row_token, inv);
+        else
+            hipLaunchKernelGGL(dispatch_scatter<false>, dim3(blocks), dim3(64 * kDispWaves), 0,
+                               s, k, ids, T, N, K, ld, hist, counts, offsets, tile_off,
+                               tail_list, plan, row_token, inv);
     }
     return hipGetLastError();
 }

@@ -15,6 +15,7 @@ HEADER = os.path.join(ROOT, "include", "elbow_moe.h")
 
 OK, INVALID, UNSUPPORTED, WORKSPACE = 0, 1, 2, 3
 DUMMY = C.c_void_p(0x1000)   # never dereferenced: every call below fails validation
+DUMMY_MISALIGNED = C.c_void_p(0x1010)
 
 
 def declared_functions():
@@ -81,6 +82,7 @@ def test_experts_validation():
     assert call(K=9) == INVALID
     assert call(ws=None) == WORKSPACE
     assert call(wsb=16) == WORKSPACE
+    assert call(ws=DUMMY_MISALIGNED) == WORKSPACE       # not 256-byte aligned
     assert call(y=None) == INVALID
     assert call(T=0, ws=None, y=None) == OK
 
@@ -102,6 +104,8 @@ def test_dispatch_and_router_validation():
                             None) == WORKSPACE
     assert lib.elb_dispatch(DUMMY, DUMMY, 100, 64, 65, DUMMY, DUMMY, DUMMY, DUMMY, DUMMY,
                             1 << 30, None) == INVALID
+    assert lib.elb_dispatch(DUMMY, DUMMY, 100, 64, 8, DUMMY, DUMMY, DUMMY, DUMMY,
+                            DUMMY_MISALIGNED, 1 << 30, None) == WORKSPACE  # not 256-byte aligned
     assert lib.elb_router_logits(DUMMY, DUMMY, 100, 100, 64, 1, DUMMY, None) == INVALID
     assert lib.elb_router_logits(DUMMY, DUMMY, 100, 128, 100, 1, DUMMY, None) == UNSUPPORTED
 
