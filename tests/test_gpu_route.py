@@ -26,6 +26,14 @@ def test_route_planted_65536x64():
     compare_routing(k, ids, w, O.route(lg, K=8), "planted 65536x64 elbow")
 
 
+def test_route_planted_2p20x64():
+    """The routing-only workload at T = 2^20 (the largest size the benchmark times, 4096 blocks of
+    16 waves per SIMD): every token against the oracle."""
+    lg = synth.planted_logits(T=1 << 20, N=64, seed=1)
+    k, ids, w = _run(lg, 8)
+    compare_routing(k, ids, w, O.route(lg, K=8), "planted 2^20x64 elbow")
+
+
 def test_route_planted_topk_is_exact_everywhere():
     lg = synth.planted_logits(T=65536, N=64, seed=1)
     k, ids, w = _run(lg, 8, mode=B.MODE_TOPK)
