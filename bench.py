@@ -101,6 +101,20 @@ def routing_only(B, torch, T=65536, N=64, K=8, nbuf=32, iters=64, big_T=0):
     out = {"workload": "routing-only T=%d N=%d K=%d planted logits" % (T, N, K),
            "kernel": "route", "us": round(us, 3), "bytes": nbytes, "GB/s": round(gbs, 1),
            "peak": PEAK_HBM_GBS, "frac": round(gbs / PEAK_HBM_GBS, 4)}
+    # the same launches back to back with one event pair around all of them: the per-launch
+    # pairs above add their own overhead (a few us) to a kernel this short
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for i in range(iters):
+        L.elb_route(C.c_void_p(bufs[i % nbuf].data_ptr()), T, N, C.byref(p),
+                    C.c_void_p(k.data_ptr()), C.c_void_p(ids.data_ptr()),
+                    C.c_void_p(w.data_ptr()), st)
+    e1.record()
+    torch.cuda.synchronize()
+    us_b = e0.elapsed_time(e1) / iters * 1e3
+    out["back_to_back"] = {"us": round(us_b, 3),
+                           "GB/s": round(nbytes / (us_b * 1e-6) / 1e9, 1),
+                           "frac": round(nbytes / (us_b * 1e-6) / 1e9 / PEAK_HBM_GBS, 4)}
     if big_T:
         # supplementary point: the same kernel on 2^20 tokens (16 waves per SIMD), two
         # 268 MB logit buffers in turn (more than the last-level cache)
@@ -127,6 +141,15 @@ def routing_only(B, torch, T=65536, N=64, K=8, nbuf=32, iters=64, big_T=0):
         out["T_2^20"] = {"us": round(us2, 2), "bytes": nb2,
                          "GB/s": round(nb2 / (us2 * 1e-6) / 1e9, 1),
                          "frac": round(nb2 / (us2 * 1e-6) / 1e9 / PEAK_HBM_GBS, 4)}
+        e0.record()
+        for i in range(16):
+            call(bufs2[i % 2])
+        e1.record()
+        torch.cuda.synchronize()
+        us2b = e0.elapsed_time(e1) / 16 * 1e3
+        out["T_2^20"]["back_to_back"] = {
+            "us": round(us2b, 2), "GB/s": round(nb2 / (us2b * 1e-6) / 1e9, 1),
+            "frac": round(nb2 / (us2b * 1e-6) / 1e9 / PEAK_HBM_GBS, 4)}
         del lg2, bufs2, k2, ids2, w2
     # variable-k dispatch of that routing (histogram, scan, scatter)
     for _ in range(4):
