@@ -7,8 +7,9 @@ combine) over one batch of synthetic OLMoE-shaped tokens already resident in HBM
 Prints ONE JSON line with tokens/s, the roofline of the dominant kernel (the grouped
 gate/up expert GEMM on MFMA), the fixed top-8 baseline through the same kernels, the
 routing kernel's and the routing variants' HBM fractions on the routing-only workload, the
-decode-sized layer (T = 64) with its expert weight stream against HBM bandwidth, and the
-fp64 CPU oracle timed on a bounded token sample on this host.
+decode-sized layer (T = 64) with its expert weight stream against HBM bandwidth, sixteen
+stacked layers with residual adds (T = 16384: end-to-end tokens/s, mean k and load CV per
+layer, elbow vs top-8), and the fp64 CPU oracle timed on a bounded token sample on this host.
 """
 from __future__ import annotations
 
