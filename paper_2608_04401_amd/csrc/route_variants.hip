@@ -7,7 +7,8 @@
 // sorting network carries the expert ids along with the logits, so the id at every rank is
 // known and any cap up to N costs the same.  Same bits as the routing kernel: the same keys,
 // u_i = exp(l_(i) - l_(0)) in rank order, S summed in rank order, the same scaled deviation
-// and first argmax, w = u * (1 / denominator).
+// and first argmax, w = u * (1 / denominator).  The elbow angle alone (no selection asked
+// for) sorts the keys only.
 #include "route_lane.h"
 
 namespace elb {
@@ -42,7 +43,10 @@ __device__ __forceinline__ void sort_pairs_desc(int64_t* v, std::integer_sequenc
     (cx_pair<NP, Q>(v), ...);
 }
 
-template <int NP, bool FULL>
+// PAIRS: sort (key, id) pairs (a selection is asked for); otherwise only the elbow index and
+// angle are, and the keys alone are sorted (the routing kernel's value network: the same
+// sorted keys, so the same e and theta bits, at two instructions per comparator)
+template <int NP, bool FULL, bool PAIRS>
 __global__ __launch_bounds__(256) void route_pair_kernel(
     const float* __restrict__ logits, const float* __restrict__ rand, int64_t T, int N, int K,
     float eps, int mode, int renorm, int vec4, XTable xt, int* __restrict__ kout,
@@ -66,19 +70,28 @@ __global__ __launch_bounds__(256) void route_pair_kernel(
     const int Nn = FULL ? NP : N;
 
     // ---- sort (key, id) pairs: rank r holds key[r] and id[r] ----
-    int64_t v[NP];
-#pragma unroll
-    for (int c = 0; c < NP; ++c) {
-        const float f = (c < Nn) ? order_key(row[c]) : -INFINITY;
-        v[c] = ((int64_t)ord_flip(__float_as_int(f)) << 32) | (uint32_t)(NP - 1 - c);
-    }
-    sort_pairs_desc<NP>(v, std::make_integer_sequence<int, NetHolder<NP>::net.n>{});
     float key[NP];
     int id[NP];
+    if (PAIRS) {
+        int64_t v[NP];
 #pragma unroll
-    for (int r = 0; r < NP; ++r) {
-        key[r] = __int_as_float(ord_flip((int)(v[r] >> 32)));
-        id[r] = NP - 1 - (int)(uint32_t)v[r];
+        for (int c = 0; c < NP; ++c) {
+            const float f = (c < Nn) ? order_key(row[c]) : -INFINITY;
+            v[c] = ((int64_t)ord_flip(__float_as_int(f)) << 32) | (uint32_t)(NP - 1 - c);
+        }
+        sort_pairs_desc<NP>(v, std::make_integer_sequence<int, NetHolder<NP>::net.n>{});
+#pragma unroll
+        for (int r = 0; r < NP; ++r) {
+            key[r] = __int_as_float(ord_flip((int)(v[r] >> 32)));
+            id[r] = NP - 1 - (int)(uint32_t)v[r];
+        }
+    } else {
+#pragma unroll
+        for (int c = 0; c < NP; ++c) {
+            key[c] = (c < Nn) ? order_key(row[c]) : -INFINITY;
+            id[c] = 0;  // not used: no selection without PAIRS
+        }
+        sort_desc<NP>(key, std::make_integer_sequence<int, NetHolder<NP>::net.n>{});
     }
 
     // ---- u, S, u_min and the elbow: the routing kernel's arithmetic, in rank order ----
@@ -123,7 +136,7 @@ __global__ __launch_bounds__(256) void route_pair_kernel(
         }
         thout[t] = th;
     }
-    if (!ids) return;
+    if (!PAIRS || !ids) return;
     const int k = (mode == ELB_MODE_TOPK) ? K : (e + 1 < K ? e + 1 : K);
     if (active) kout[t] = k;
 
@@ -221,9 +234,15 @@ void launch_pair_np(const float* logits, const float* rand, int64_t T, int N,
                     hipStream_t s) {
     const int64_t waves = (T + kWave - 1) / kWave;
     const int vec4 = ((uintptr_t)logits % 16) == 0;
-    hipLaunchKernelGGL((route_pair_kernel<NP, FULL>), dim3((unsigned)((waves + 3) / 4)),
-                       dim3(256), 0, s, logits, rand, T, N, p.K, p.eps, p.mode, p.renormalize,
-                       vec4, make_xtable(N), k, ids, w, e, theta);
+    const dim3 grid((unsigned)((waves + 3) / 4));
+    if (ids)
+        hipLaunchKernelGGL((route_pair_kernel<NP, FULL, true>), grid, dim3(256), 0, s, logits,
+                           rand, T, N, p.K, p.eps, p.mode, p.renormalize, vec4, make_xtable(N),
+                           k, ids, w, e, theta);
+    else
+        hipLaunchKernelGGL((route_pair_kernel<NP, FULL, false>), grid, dim3(256), 0, s, logits,
+                           nullptr, T, N, p.K, p.eps, p.mode, p.renormalize, vec4,
+                           make_xtable(N), k, nullptr, w, e, theta);
 }
 
 }  // namespace
