@@ -7,8 +7,8 @@
 // sorting network carries the expert ids along with the logits, so the id at every rank is
 // known and any cap up to N costs the same.  Same bits as the routing kernel: the same keys,
 // u_i = exp(l_(i) - l_(0)) in rank order, S summed in rank order, the same scaled deviation
-// and first argmax, w = u * (1 / denominator).  The elbow angle alone (no selection asked
-// for) sorts the keys only.
+// and first argmax, w = u * (1 / denominator).  The elbow angle (no selection asked for) and
+// tail randomisation with K <= 16 sort the keys only.
 #include "route_lane.h"
 
 namespace elb {
@@ -43,9 +43,70 @@ __device__ __forceinline__ void sort_pairs_desc(int64_t* v, std::integer_sequenc
     (cx_pair<NP, Q>(v), ...);
 }
 
-// PAIRS: sort (key, id) pairs (a selection is asked for); otherwise only the elbow index and
-// angle are, and the keys alone are sorted (the routing kernel's value network: the same
-// sorted keys, so the same e and theta bits, at two instructions per comparator)
+// The experts of the first k ranks from the sorted keys, by the routing kernel's rule
+// (tau = the key at rank k - 1; every key above tau, then keys equal to tau by lowest id):
+// their mask `taken`, and up to KM of them in id order (cid) with their keys (ck, -inf past k;
+// re-read from the token's LDS row, as the id is not a compile-time constant there).
+template <int NP, int KM>
+__device__ __forceinline__ void first_k_experts(const float (&key)[NP], const float (&okey)[NP],
+                                                const float* row, int Nn, int k,
+                                                uint64_t& taken, int (&cid)[KM],
+                                                float (&ck)[KM]) {
+    float tau = key[0];
+#pragma unroll
+    for (int i = 0; i < KM; ++i)
+        if (i == k - 1) tau = key[i];
+    int g = 0;
+#pragma unroll
+    for (int i = 0; i < KM; ++i)
+        if (i < k && key[i] > tau) ++g;
+    uint32_t sel_lo = 0, sel_hi = 0;
+#pragma unroll
+    for (int c = 0; c < NP; ++c) {
+        const uint32_t bit = (c < Nn && okey[c] >= tau) ? (1u << (c & 31)) : 0u;
+        if (c < 32) sel_lo |= bit;
+        else sel_hi |= bit;
+    }
+    const bool tie = (__popc(sel_lo) + __popc(sel_hi)) != k;
+    if (__any(tie)) {  // wave-uniform slow path: ties at tau, lowest ids first
+        uint32_t eq_lo = 0, eq_hi = 0;
+        sel_lo = sel_hi = 0;
+#pragma unroll
+        for (int c = 0; c < NP; ++c) {
+            const uint32_t bit = 1u << (c & 31);
+            const bool real = c < Nn;
+            const uint32_t gt = (real && okey[c] > tau) ? bit : 0u;
+            const uint32_t eq = (real && okey[c] == tau) ? bit : 0u;
+            if (c < 32) {
+                sel_lo |= gt;
+                eq_lo |= eq;
+            } else {
+                sel_hi |= gt;
+                eq_hi |= eq;
+            }
+        }
+        for (int r = 0; r < k - g; ++r) {
+            const int b = lowest_bit(eq_lo, eq_hi);
+            if (b < 32) { sel_lo |= 1u << b; eq_lo &= ~(1u << b); }
+            else { sel_hi |= 1u << (b - 32); eq_hi &= ~(1u << (b - 32)); }
+        }
+    }
+    taken = ((uint64_t)sel_hi << 32) | sel_lo;
+#pragma unroll
+    for (int r = 0; r < KM; ++r) {
+        const int b = lowest_bit(sel_lo, sel_hi);
+        cid[r] = b;
+        ck[r] = r < k ? order_key(row[b]) : -INFINITY;
+        if (b < 32) sel_lo &= sel_lo - 1;
+        else sel_hi &= sel_hi - 1;
+    }
+}
+
+// PAIRS: sort (key, id) pairs (a selection with any cap is asked for).  Otherwise the keys
+// alone are sorted (the routing kernel's value network: the same sorted keys, so the same e
+// and theta bits, at two instructions per comparator): for the elbow angle (no selection), and
+// for tail randomisation with K <= kLaneMaxK, whose first k experts are then recovered by the
+// routing kernel's selection rule.
 template <int NP, bool FULL, bool PAIRS>
 __global__ __launch_bounds__(256) void route_pair_kernel(
     const float* __restrict__ logits, const float* __restrict__ rand, int64_t T, int N, int K,
@@ -136,9 +197,70 @@ __global__ __launch_bounds__(256) void route_pair_kernel(
         }
         thout[t] = th;
     }
-    if (!PAIRS || !ids) return;
+    if (!ids) return;
     const int k = (mode == ELB_MODE_TOPK) ? K : (e + 1 < K ? e + 1 : K);
     if (active) kout[t] = k;
+
+    if (!PAIRS) {
+        // tail randomisation with K <= kLaneMaxK from the sorted keys alone: the first k ranks'
+        // experts by the routing kernel's selection rule, then the K - k untaken experts with
+        // the smallest draws (equal draws: lower id), as below; the same ids and weight bits
+        // as the pair path (an elbow expert's u is recomputed from its own key)
+        constexpr int KM = NP < kLaneMaxK ? NP : kLaneMaxK;
+        float okey[NP];
+#pragma unroll
+        for (int c = 0; c < NP; ++c) okey[c] = (c < Nn) ? order_key(row[c]) : -INFINITY;
+        uint64_t taken;
+        int cid[KM];
+        float ck[KM];
+        first_k_experts<NP, KM>(key, okey, row, Nn, k, taken, cid, ck);
+        const float* rr = rand + t * N;
+        float draw[NP];
+#pragma unroll
+        for (int c = 0; c < NP; ++c) draw[c] = (c < Nn) ? rr[c] : INFINITY;
+        float denom = S;
+        if (renorm) {
+            denom = 0.f;
+#pragma unroll
+            for (int j = 0; j < KM; ++j)
+                if (j < k) denom += u[j];
+        }
+        for (int j = k; j < K; ++j) {
+            float bv = INFINITY;
+            int bc = -1;
+#pragma unroll
+            for (int c = 0; c < NP; ++c) {
+                const bool ok = c < Nn && !((taken >> c) & 1ull) && (bc < 0 || draw[c] < bv);
+                bv = ok ? draw[c] : bv;
+                bc = ok ? c : bc;
+            }
+            taken |= 1ull << bc;
+            const float ub = __builtin_amdgcn_exp2f((order_key(row[bc]) - lmax) * kLog2e);
+            if (active) {
+                ids[t * K + j] = bc;
+                wout[t * K + j] = ub;
+            }
+            if (renorm) denom += ub;
+        }
+        const float inv = 1.0f / denom;
+        if (!active) return;
+        // the elbow's experts at their ranks (descending key; equal keys: lower id first)
+#pragma unroll
+        for (int r = 0; r < KM; ++r) {
+            if (r < k) {
+                int rank = 0;
+#pragma unroll
+                for (int q = 0; q < KM; ++q) {
+                    if (q < r) rank += (q < k && ck[q] >= ck[r]) ? 1 : 0;
+                    if (q > r) rank += (q < k && ck[q] > ck[r]) ? 1 : 0;
+                }
+                ids[t * K + rank] = cid[r];
+                wout[t * K + rank] = __builtin_amdgcn_exp2f((ck[r] - lmax) * kLog2e) * inv;
+            }
+        }
+        for (int j = k; j < K; ++j) wout[t * K + j] *= inv;  // this lane's own writes
+        return;
+    }
 
     if (rand) {
         // tail randomisation: K - k experts outside the first k ranks, smallest draws first
@@ -235,14 +357,16 @@ void launch_pair_np(const float* logits, const float* rand, int64_t T, int N,
     const int64_t waves = (T + kWave - 1) / kWave;
     const int vec4 = ((uintptr_t)logits % 16) == 0;
     const dim3 grid((unsigned)((waves + 3) / 4));
-    if (ids)
+    // keys only: the elbow angle (no ids), or tail randomisation with K <= kLaneMaxK
+    const bool keys_only = !ids || (rand && p.K <= kLaneMaxK);
+    if (!keys_only)
         hipLaunchKernelGGL((route_pair_kernel<NP, FULL, true>), grid, dim3(256), 0, s, logits,
                            rand, T, N, p.K, p.eps, p.mode, p.renormalize, vec4, make_xtable(N),
                            k, ids, w, e, theta);
     else
         hipLaunchKernelGGL((route_pair_kernel<NP, FULL, false>), grid, dim3(256), 0, s, logits,
-                           nullptr, T, N, p.K, p.eps, p.mode, p.renormalize, vec4,
-                           make_xtable(N), k, nullptr, w, e, theta);
+                           rand, T, N, p.K, p.eps, p.mode, p.renormalize, vec4,
+                           make_xtable(N), k, ids, w, e, theta);
 }
 
 }  // namespace
