@@ -361,6 +361,14 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
     // Copy sources: wave w copies rows [64w, 64w + 64) of each tile, 8 rows (1 KB) per
     // instruction; lane l fills physical chunk l & 7 of row 64w + 8i + (l >> 3), so it
     // fetches that row's logical chunk swz8(row, l & 7) (the XOR is its own inverse).
+    // The copy instruction adds a 32-bit per-lane byte offset to a 64-bit scalar base, so the
+    // bases are per block: the expert's weight matrix, and in the down GEMM the tile's first
+    // H row.  The offsets then stay below one expert's weights (2 m d or d m elements) or 256
+    // H rows; only the gathered x rows of the gate/up GEMM are addressed from x itself, and
+    // gemm_tile_rows sends a problem to this kernel only when T d elements take less than
+    // 2^32 bytes.
+    const bf16_t* const Ablk = (MODE == 0) ? A : A + (int64_t)row0 * m;
+    const bf16_t* const Bblk = B + (int64_t)e * ((MODE == 0) ? 2 * m : d) * Kd;
     uint32_t a_off[8], b_off[8];  // element offsets of each row's chunk (k = 0)
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
@@ -371,12 +379,12 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
             a_off[i] = (uint32_t)row_token[row0 + rr] * (uint32_t)d + c * 8;
             const int hc = ntile * 128;
             const int brow = (r < 128) ? (hc + r) : (m + hc + (r - 128));
-            b_off[i] = ((uint32_t)e * 2u * (uint32_t)m + brow) * (uint32_t)d + c * 8;
+            b_off[i] = (uint32_t)brow * (uint32_t)d + c * 8;
         } else {
-            a_off[i] = (uint32_t)(row0 + rr) * (uint32_t)m + c * 8;
+            a_off[i] = (uint32_t)rr * (uint32_t)m + c * 8;
             int brow = ntile * TN + r;
             brow = brow < d ? brow : d - 1;
-            b_off[i] = ((uint32_t)e * (uint32_t)d + brow) * (uint32_t)m + c * 8;
+            b_off[i] = (uint32_t)brow * (uint32_t)m + c * 8;
         }
     }
     // LDS byte address of this wave's first 8-row group in unit 0
@@ -470,13 +478,13 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
     // every copy in flight.
     const int nk = Kd / TK;  // >= 1
     // as if barriers at t = -3, -2, -1 had issued B(0); A(0), B(1); A(1), B(2)
-    issue(B, b_off, 0, 0, true);
-    issue(A, a_off, 1, 0, false);
+    issue(Bblk, b_off, 0, 0, true);
+    issue(Ablk, a_off, 1, 0, false);
     if (nk > 1) {
-        issue(B, b_off, 2, TK, true);
-        issue(A, a_off, 3, TK, false);
+        issue(Bblk, b_off, 2, TK, true);
+        issue(Ablk, a_off, 3, TK, false);
         if (nk > 2) {
-            issue(B, b_off, 4, 2 * TK, true);
+            issue(Bblk, b_off, 4, 2 * TK, true);
             ELB_WAIT_VMCNT(24);
         } else {
             ELB_WAIT_VMCNT(16);
@@ -520,9 +528,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
             if ((q & 1) == 1) {
                 const int i = q >> 1;
                 if (i < 8) {
-                    if (t + 2 < nk) issue_one(A, a_off, ub, (t + 2) * TK, false, i);  // -> unit 2t
+                    if (t + 2 < nk) issue_one(Ablk, a_off, ub, (t + 2) * TK, false, i);  // -> unit 2t
                 } else {
-                    if (t + 3 < nk) issue_one(B, b_off, ua, (t + 3) * TK, true, i - 8);
+                    if (t + 3 < nk) issue_one(Bblk, b_off, ua, (t + 3) * TK, true, i - 8);
                 }
                 __builtin_amdgcn_sched_barrier(0);
             }
@@ -684,7 +692,12 @@ unsigned grid8(int64_t blocks) { return (unsigned)((blocks + 7) / 8 * 8); }
 int gemm_tile_rows(int dtype, int64_t T, int K, int N, int d, int m) {
     if (dtype != ELB_BF16) return FBM;
     const int64_t avg_rows = T * K / (N > 0 ? N : 1);
-    return (m % 128 == 0 && d >= 128 && T > 0 && avg_rows >= 192) ? LBM : BM;
+    // the large-tile kernel's 32-bit byte offsets: gathered x rows from x itself (T d
+    // elements), weights from the expert's own matrix (2 m d elements); larger problems take
+    // the 128-row kernel, which addresses with 64-bit pointers
+    const bool offsets_fit = (uint64_t)T * (uint64_t)d * 2u < ((uint64_t)1 << 32) &&
+                             (uint64_t)m * (uint64_t)d * 4u < ((uint64_t)1 << 32);
+    return (m % 128 == 0 && d >= 128 && T > 0 && avg_rows >= 192 && offsets_fit) ? LBM : BM;
 }
 
 hipError_t launch_gemm_gate_up(const void* x, const void* Wgu, const int* row_token,
