@@ -1,7 +1,8 @@
 """GPU parity of the 16-layer residual stack at full size: 16 OLMoE-shaped layers (d=2048,
 N=64 experts, SwiGLU intermediate 1024, bf16), T=16384 tokens, h <- h + MoE_l(h), elbow
-routing capped at K=8.  Every layer runs on all 16384 tokens; a seeded sample of tokens is
-checked against the fp64 oracle layer by layer on the same input (teacher-forced: the oracle
+routing capped at K=8.  Every layer runs on all 16384 tokens; every token's routing is
+checked against the oracle's on that layer's own fp32 logits, and a seeded sample of 512
+tokens is checked against the fp64 oracle layer by layer on the same input (teacher-forced: the oracle
 layer gets the GPU's bf16 input rows, since tokens are independent through the stack and one
 near-tie flip would change every later layer).  Weights are drawn on the device
 (synth.device_stack_layer); the oracle reads host copies of the same tensors."""
@@ -13,19 +14,22 @@ from oracle import oracle as O
 from paper_2608_04401_amd import binding as B
 from paper_2608_04401_amd import synth
 
-from helpers import NEAR_TIE, RTOL_BF16, cpu, rel_err_rows
+from helpers import RTOL_BF16, compare_routing, cpu, rel_err_rows
 
 pytestmark = pytest.mark.gpu
 
 T, D, N, M, K, LAYERS = 16384, 2048, 64, 1024, 8, 16
 
 
+SAMPLE = 512  # tokens per layer compared with the oracle's layer (teacher-forced)
+
+
 def test_residual_stack_16_layers_sampled():
     rng = np.random.default_rng(16)
-    sample = np.sort(rng.choice(T, 24, replace=False))
+    sample = np.sort(rng.choice(T, SAMPLE, replace=False))
     sample_t = torch.from_numpy(sample).cuda()
     h = synth.device_stack_input(T, D)
-    worst, near_total, ks = 0.0, 0, []
+    worst, near_total, ks = 0.0, [], []
     for l in range(LAYERS):
         Wr, Wgu, Wd = synth.device_stack_layer(l, D, N, M)
         y, dbg = B.elb_moe_forward(h, Wr, Wgu, Wd, K=K, residual=h, debug=True)
@@ -33,17 +37,24 @@ def test_residual_stack_16_layers_sampled():
         k = cpu(dbg["k"])
         assert ((k >= 1) & (k <= K)).all()
         ks.append(float(k.mean()))
+        # every token's routing against the oracle on this layer's own fp32 logits
+        r = O.route(cpu(dbg["logits"]), K=K)
+        near, _ = compare_routing(dbg["k"], dbg["ids"], dbg["w"], r, "stack layer %d" % l)
+        near_total.append(near)
+        # the sampled tokens' outputs against the oracle's layer on the same bf16 inputs
         hs = cpu(h.index_select(0, sample_t))
         ref = O.moe_forward(hs, cpu(Wr), cpu(Wgu), cpu(Wd), K=K, residual=hs)
-        near = ref.routing.margin < NEAR_TIE
+        ids = cpu(dbg["ids"])
+        same = (k[sample] == ref.routing.k) & (ids[sample] == ref.routing.ids).all(axis=1)
+        # routed differently only within the fp32 logits' rounding of a tie (|dD| <= 16 max|dl|)
+        dl = float(np.abs(cpu(dbg["logits"])[sample] - ref.logits).max())
+        tie64 = max(1e-6, 32.0 * dl)
+        assert (ref.routing.margin[~same] < tie64).all(), "layer %d: routing differs" % l
         rel = rel_err_rows(cpu(y.index_select(0, sample_t)), ref.y)
-        assert rel[~near].max() < RTOL_BF16, "layer %d: max rel err %.3g" % (l, rel[~near].max())
-        gk = k[sample]
-        assert np.array_equal(gk[~near], ref.routing.k[~near]), "layer %d: k differs" % l
-        worst = max(worst, float(rel[~near].max()))
-        near_total += int(near.sum())
+        assert rel[same].max() < RTOL_BF16, "layer %d: max rel err %.3g" % (l, rel[same].max())
+        worst = max(worst, float(rel[same].max()))
         h = y
         del Wr, Wgu, Wd, dbg
-    print("16-layer stack: sampled tokens %d per layer, max rel err %.2e, near-ties %d, "
-          "mean k per layer %s" % (len(sample), worst, near_total,
-                                   " ".join("%.3f" % v for v in ks)))
+    print("16-layer stack: %d sampled tokens per layer, max rel err %.2e, near-ties per layer "
+          "%s, mean k per layer %s" % (len(sample), worst, near_total,
+                                       " ".join("%.3f" % v for v in ks)))

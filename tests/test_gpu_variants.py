@@ -229,3 +229,24 @@ def test_tail_random_topk_mode_has_no_tail():
     r = O.route(lg, K=8, mode=O.MODE_TOPK)
     torch.cuda.synchronize()
     assert (cpu(k) == 8).all() and np.array_equal(cpu(ids), r.ids)
+
+
+@pytest.mark.parametrize("N", [16, 37, 64])
+@pytest.mark.parametrize("K", [8, 16])
+def test_tail_random_tied_and_neg_inf_logits(N, K):
+    """Logits that tie at the selection boundary (quantised values, so rank k - 1 often has
+    equal keys that only the lower-id rule separates) and -inf logits, for the caps that sort
+    the keys alone (K <= 16): the elbow's experts and their weights must be the routing's."""
+    if K > N:
+        pytest.skip("K > N")
+    rng = np.random.default_rng(N * 100 + K)
+    T = 6000
+    lg = (np.round(rng.standard_normal((T, N)) * 2) / 2).astype(np.float32)
+    lg[:64] = 0.5                                # all equal: k = 1, the lowest id
+    lg[64:128, : N // 2] = 1.0                   # a flat head of N / 2 equal logits
+    lg[128::5, 3] = -np.inf
+    lg[129::9, : N - 2] = -np.inf                # only two finite logits
+    rand = (np.round(rng.random((T, N)) * 8) / 8).astype(np.float32)  # tied draws too
+    for renorm in (False, True):
+        _check_tail(lg, rand, K, renorm, "tied/-inf logits N=%d K=%d renorm=%d"
+                    % (N, K, renorm))

@@ -136,3 +136,27 @@ def test_table1_sign_convention():
     rep = stats.load_balance_report(ce, ct, K=4, T=10)
     assert rep["top1_share_change_pct"] < 0
     assert rep["cv_change_pct"] <= 0
+
+
+def test_cv_hand_value_and_textbook_definition():
+    """Appendix A.3, Corollary 2 writes CV^2 = N ||q||^2 - 1 for a utilisation vector q.  Hand
+    value: counts (2, 1, 1, 0) give q = (1/2, 1/4, 1/4, 0), mean 1/4, population variance
+    ((1/4)^2 + 0 + 0 + (1/4)^2) / 4 = 1/32, so CV^2 = (1/32) / (1/4)^2 = 1/2.  On random
+    vectors the value must equal the textbook ratio of numpy's population standard deviation
+    to the mean, and it must be 0 for uniform load."""
+    q = stats.utilization([2, 1, 1, 0])
+    assert np.array_equal(q, [0.5, 0.25, 0.25, 0.0])
+    assert abs(stats.cv2(q) - 0.5) < 1e-15
+    assert abs(stats.cv(q) - np.sqrt(0.5)) < 1e-15
+    assert stats.cv(stats.utilization([7, 7, 7, 7, 7])) < 1e-7  # sqrt of a rounding residue
+    rng = np.random.default_rng(5)
+    for N in (2, 3, 8, 64):
+        c = rng.integers(0, 1000, N) + 1
+        qq = stats.utilization(c)
+        assert abs(stats.cv(qq) - np.std(qq) / np.mean(qq)) < 1e-12
+    # Table 1 sign on a case where both CVs are non-zero: the elbow routing's more skewed load
+    # (CV 0.5 vs 0.25) is a negative % change of -100
+    ct, ce = np.array([5, 3, 3, 5]), np.array([2, 1, 1, 0])
+    rep = stats.load_balance_report(ce, ct, K=4, T=4)
+    assert abs(rep["cv_top"] - 0.25) < 1e-15 and abs(rep["cv_elbow"] - np.sqrt(0.5)) < 1e-15
+    assert abs(rep["cv_change_pct"] - (0.25 - np.sqrt(0.5)) / 0.25 * 100) < 1e-9
