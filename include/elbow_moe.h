@@ -244,9 +244,22 @@ int elb_moe_forward_packed(const void *x, const void *W_router, const void *W_ga
                            int32_t *ids_out, float *w_out, int32_t *counts_out, void *stream);
 
 /*
+ * Calibration of the matrix-core roofline (a measurement aid, not part of the layer): a
+ * kernel of `blocks` blocks of 4 waves, each wave issuing iters x 8 back-to-back
+ * v_mfma_f32_32x32x16_bf16 instructions (32 x 32 x 16 multiply-adds each) on register
+ * operands, with no memory traffic.  Timing it gives the bf16 MFMA rate the chip sustains,
+ * clock and power included.
+ *   out [blocks * 4] float   device output (one sum per wave, so the work is kept)
+ * Returns the number of MFMA instructions enqueued (> 0), or a negative elb_status.
+ */
+int64_t elb_calibrate_mfma_bf16(int32_t blocks, int32_t iters, float *out, void *stream);
+
+/*
  * Per-kernel timing (host-side hipEvents around each launch the library makes).
  * elb_profile_enable(1) starts recording on the calling process; every launch then
- * records a start/stop event pair on its stream.  elb_profile_read() synchronises on the
+ * records a start/stop event pair on its stream (events without the system-scope fence, so
+ * that recording them does not flush caches between kernels and slow the kernel that
+ * follows).  elb_profile_read() synchronises on the
  * recorded events, fills up to `cap` entries of names (static strings), total
  * milliseconds and launch counts per kernel, clears the records and returns the number
  * of kernels (or a negative elb_status).  Not for use under graph capture.

@@ -69,6 +69,7 @@ def lib():
         "elb_moe_forward_packed": ([P, P, P, P, P, P, I64, I32, I32, I32, I32,
                                     C.POINTER(RouteParams), P, P, SZ, P, P, P, P, P, P],
                                    C.c_int),
+        "elb_calibrate_mfma_bf16": ([I32, I32, P, P], C.c_int64),
         "elb_profile_enable": ([C.c_int], C.c_int),
         "elb_profile_read": ([C.POINTER(C.c_char_p), C.POINTER(C.c_double),
                               C.POINTER(C.c_int64), C.c_int], C.c_int),
@@ -299,6 +300,51 @@ def elb_moe_forward(x, W_router, W_gate_up, W_down, K: int = 8, eps: float = 1e-
             _ptr(x), _ptr(W_router), _ptr(W_gate_up), _ptr(W_down), _ptr(packed),
             _ptr(residual), T, d, N, m, dt, C.byref(p), _ptr(y), _ptr(ws), ws.numel(), *tail))
     return (y, dbg) if debug else y
+
+
+def elb_moe_forward_prepared(x, W_router, W_gate_up, W_down, K: int = 8, eps: float = 1e-8,
+                             mode: int = MODE_ELBOW, renormalize: bool = False, residual=None,
+                             out=None, packed=None):
+    """elb_moe_forward with its arguments marshalled once: returns (call, y), where call() enqueues
+    the layer on the stream that was current here and raises on a failed status.  For timing
+    loops, where the per-call argument checks would otherwise add host time."""
+    _dev(x, W_router, W_gate_up, W_down, residual, out, packed)
+    T, d = x.shape
+    N = W_router.shape[0]
+    m = W_down.shape[2]
+    dt = _dtype_code(x)
+    y = torch.empty_like(x) if out is None else out
+    ws = workspace(elb_moe_workspace_bytes(T, d, N, m, K, dt), x.device)
+    p = RouteParams(K, eps, mode, int(renormalize))
+    L = lib()
+    if packed is None:
+        fn, name = L.elb_moe_forward, "elb_moe_forward"
+        args = (_ptr(x), _ptr(W_router), _ptr(W_gate_up), _ptr(W_down), _ptr(residual), T, d, N,
+                m, dt, C.byref(p), _ptr(y), _ptr(ws), ws.numel(), None, None, None, None, None,
+                _stream())
+    else:
+        fn, name = L.elb_moe_forward_packed, "elb_moe_forward_packed"
+        args = (_ptr(x), _ptr(W_router), _ptr(W_gate_up), _ptr(W_down), _ptr(packed),
+                _ptr(residual), T, d, N, m, dt, C.byref(p), _ptr(y), _ptr(ws), ws.numel(), None,
+                None, None, None, None, _stream())
+    keep = (p, ws, y)  # referenced by the closure: the parameter block and buffers stay alive
+
+    def call():
+        rc = fn(*args)
+        if rc != 0:
+            _check(name, rc)
+        return keep
+    return call, y
+
+
+def elb_calibrate_mfma_bf16(blocks: int, iters: int) -> int:
+    """Enqueue the back-to-back MFMA calibration kernel; returns the MFMA instruction count
+    (each v_mfma_f32_32x32x16_bf16 is 32 * 32 * 16 * 2 FLOPs)."""
+    out = torch.empty(blocks * 4, dtype=torch.float32, device="cuda")
+    n = lib().elb_calibrate_mfma_bf16(blocks, iters, _ptr(out), _stream())
+    if n < 0:
+        _check("elb_calibrate_mfma_bf16", -n)
+    return int(n)
 
 
 def elb_profile_enable(on: bool = True) -> None:

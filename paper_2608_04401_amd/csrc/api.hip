@@ -148,8 +148,10 @@ hipEvent_t pool_get() {
         g_pool.pop_back();
         return e;
     }
+    // timing only: without the system-scope fence an event does not write back and
+    // invalidate the caches, which would slow the kernel that follows it
     hipEvent_t e = nullptr;
-    if (hipEventCreate(&e) != hipSuccess) return nullptr;
+    if (hipEventCreateWithFlags(&e, hipEventDisableSystemFence) != hipSuccess) return nullptr;
     return e;
 }
 
@@ -477,6 +479,17 @@ int elb_pack_expert_weights(const void* W_gate_up, const void* W_down, int32_t N
     return hip_status(launch_pack_experts(W_gate_up, W_down, N, d, m, packed,
                                           (hipStream_t)stream),
                       "pack_experts");
+}
+
+int64_t elb_calibrate_mfma_bf16(int32_t blocks, int32_t iters, float* out, void* stream) {
+    g_err.clear();
+    if (blocks < 1 || iters < 1)
+        return -fail(ELB_ERR_INVALID_ARG, "blocks = %d and iters = %d must be >= 1", blocks, iters);
+    if (!out) return -fail(ELB_ERR_INVALID_ARG, "NULL tensor pointer");
+    if (int rc = hip_status(launch_calibrate_mfma(blocks, iters, out, (hipStream_t)stream),
+                            "calibrate_mfma"))
+        return -rc;
+    return (int64_t)blocks * 4 * iters * 8;
 }
 
 int elb_profile_enable(int on) {

@@ -117,6 +117,9 @@ hipError_t launch_combine(const void* Y, const int* k, const int* inv, const flo
                           const void* residual, int64_t T, int d, int K, int dtype, void* y,
                           hipStream_t s);
 
+// calibration: back-to-back bf16 MFMAs, blocks x 4 waves x iters x 8 of them; out [blocks * 4]
+hipError_t launch_calibrate_mfma(int blocks, int iters, float* out, hipStream_t s);
+
 // ---- per-kernel timing hooks (api.hip) ----
 struct ProfileScope {
     ProfileScope(const char* name, hipStream_t s);
