@@ -213,6 +213,33 @@ int elb_moe_forward(const void *x, const void *W_router, const void *W_gate_up,
                     void *stream);
 
 /*
+ * The whole layer (elb_moe_forward) without a caller workspace and without any allocation,
+ * for callers that cannot allocate device memory: code under HIP graph capture, tight serving
+ * loops, harnesses that forbid hipMalloc.  Scratch comes from a static device array of
+ * ELB_NOALLOC_SCRATCH_BYTES per GPU (256 MiB, held by every GPU the library runs on until the
+ * process ends; its address is looked up once per device, on the first call there, with the
+ * stream's device current).  The caller still passes inputs and outputs, as for
+ * elb_moe_forward, whose kernels and results (bit for bit) this call shares.
+ * Limits and behaviour:
+ *  - a problem whose elb_moe_workspace_bytes(T, d, N, m, K, dtype) exceeds
+ *    ELB_NOALLOC_SCRATCH_BYTES is rejected with ELB_ERR_UNSUPPORTED before anything is
+ *    enqueued (the OLMoE-shaped layer, d = 2048, N = 64, m = 1024, K = 8, fits up to about
+ *    5400 tokens);
+ *  - nothing in the scratch has to start at zero, and nothing is cleared;
+ *  - every call on one GPU uses that GPU's one array, so calls that overlap in time on one
+ *    GPU (different streams, or different host threads) race and must be serialised by the
+ *    caller; calls in order on one stream are safe;
+ *  - with elb_profile_enable(1) the library creates timing events; leave profiling off where
+ *    no allocation of any kind is allowed.
+ */
+#define ELB_NOALLOC_SCRATCH_BYTES ((size_t)256 << 20)
+int elb_moe_forward_noalloc(const void *x, const void *W_router, const void *W_gate_up,
+                            const void *W_down, const void *residual, int64_t T, int32_t d,
+                            int32_t N, int32_t m, int32_t dtype, const elb_route_params *params,
+                            void *y, float *logits_out, int32_t *k_out, int32_t *ids_out,
+                            float *w_out, int32_t *counts_out, void *stream);
+
+/*
  * Packed expert weights for decode-sized batches.  When an expert gets at most 16 rows on
  * average (T K <= 16 N), the expert GEMMs are bound by reading the weights; the layer then
  * streams each expert's weights in 64-row tasks.  elb_pack_expert_weights writes a copy of

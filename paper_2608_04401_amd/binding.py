@@ -69,6 +69,8 @@ def lib():
         "elb_moe_forward_packed": ([P, P, P, P, P, P, I64, I32, I32, I32, I32,
                                     C.POINTER(RouteParams), P, P, SZ, P, P, P, P, P, P],
                                    C.c_int),
+        "elb_moe_forward_noalloc": ([P, P, P, P, P, I64, I32, I32, I32, I32,
+                                     C.POINTER(RouteParams), P, P, P, P, P, P, P], C.c_int),
         "elb_calibrate_mfma_bf16": ([I32, I32, P, P], C.c_int64),
         "elb_profile_enable": ([C.c_int], C.c_int),
         "elb_profile_read": ([C.POINTER(C.c_char_p), C.POINTER(C.c_double),
@@ -299,6 +301,35 @@ def elb_moe_forward(x, W_router, W_gate_up, W_down, K: int = 8, eps: float = 1e-
         _check("elb_moe_forward_packed", lib().elb_moe_forward_packed(
             _ptr(x), _ptr(W_router), _ptr(W_gate_up), _ptr(W_down), _ptr(packed),
             _ptr(residual), T, d, N, m, dt, C.byref(p), _ptr(y), _ptr(ws), ws.numel(), *tail))
+    return (y, dbg) if debug else y
+
+
+NOALLOC_SCRATCH_BYTES = 256 << 20
+
+
+def elb_moe_forward_noalloc(x, W_router, W_gate_up, W_down, K: int = 8, eps: float = 1e-8,
+                            mode: int = MODE_ELBOW, renormalize: bool = False, residual=None,
+                            out=None, debug: bool = False):
+    """The whole layer through the allocation-free entry point (the library's static scratch,
+    no workspace).  Returns y, or (y, dict of intermediates) when debug=True."""
+    _dev(x, W_router, W_gate_up, W_down, residual, out)
+    T, d = x.shape
+    N = W_router.shape[0]
+    m = W_down.shape[2]
+    dev = x.device
+    y = torch.empty_like(x) if out is None else out
+    dbg = {}
+    if debug:
+        dbg = {"logits": torch.empty((T, N), dtype=torch.float32, device=dev),
+               "k": torch.empty(T, dtype=torch.int32, device=dev),
+               "ids": torch.empty((T, K), dtype=torch.int32, device=dev),
+               "w": torch.empty((T, K), dtype=torch.float32, device=dev),
+               "counts": torch.empty(N, dtype=torch.int32, device=dev)}
+    p = RouteParams(K, eps, mode, int(renormalize))
+    _check("elb_moe_forward_noalloc", lib().elb_moe_forward_noalloc(
+        _ptr(x), _ptr(W_router), _ptr(W_gate_up), _ptr(W_down), _ptr(residual), T, d, N, m,
+        _dtype_code(x), C.byref(p), _ptr(y), _ptr(dbg.get("logits")), _ptr(dbg.get("k")),
+        _ptr(dbg.get("ids")), _ptr(dbg.get("w")), _ptr(dbg.get("counts")), _stream()))
     return (y, dbg) if debug else y
 
 

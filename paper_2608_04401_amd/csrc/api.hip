@@ -132,6 +132,34 @@ int check_expert_dims(int64_t T, int d, int N, int m, int K, int dtype) {
     return ELB_OK;
 }
 
+// ---- the static scratch of the allocation-free entry point ----
+// One array per GPU the library runs on (a __device__ variable lives in each device's copy of
+// the code object).  In host code `scratch` is only a stand-in symbol: its device address is
+// looked up with hipGetSymbolAddress, once per device with that device current, and only that
+// address is passed to kernels.
+constexpr size_t kScratchBytes = (size_t)ELB_NOALLOC_SCRATCH_BYTES;
+static __device__ __attribute__((aligned(256))) char scratch[kScratchBytes];
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[64] = {};
+
+int scratch_address(void** out) {
+    int dev = 0;
+    if (hipError_t e = hipGetDevice(&dev)) return hip_status(e, "hipGetDevice");
+    if (dev < 0 || dev >= 64) return fail(ELB_ERR_UNSUPPORTED, "device index %d >= 64", dev);
+    std::lock_guard<std::mutex> lk(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void* p = nullptr;
+        const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return hip_status(e, "hipGetSymbolAddress(scratch)");
+        if (!p || (uintptr_t)p % kAlign)
+            return fail(ELB_ERR_HIP, "scratch address %p is null or not %zu-byte aligned", p,
+                        kAlign);
+        g_scratch_ptr[dev] = p;
+    }
+    *out = g_scratch_ptr[dev];
+    return ELB_OK;
+}
+
 // ---- per-kernel timing ----
 struct Rec {
     const char* name;
@@ -458,6 +486,30 @@ int elb_moe_forward_packed(const void* x, const void* W_router, const void* W_ga
     return moe_forward_entry(x, W_router, W_gate_up, W_down, packed, residual, T, d, N, m,
                              dtype, params, y, workspace, workspace_bytes, logits_out, k_out,
                              ids_out, w_out, counts_out, stream);
+}
+
+int elb_moe_forward_noalloc(const void* x, const void* W_router, const void* W_gate_up,
+                            const void* W_down, const void* residual, int64_t T, int32_t d,
+                            int32_t N, int32_t m, int32_t dtype, const elb_route_params* params,
+                            void* y, float* logits_out, int32_t* k_out, int32_t* ids_out,
+                            float* w_out, int32_t* counts_out, void* stream) {
+    g_err.clear();
+    // every size check before any HIP call: an oversized problem is rejected on the host
+    if (int rc = check_route_params(N, params)) return rc;
+    if (int rc = check_expert_dims(T, d, N, m, params->K, dtype)) return rc;
+    if (T == 0) return ELB_OK;
+    if (!x || !W_router || !W_gate_up || !W_down || !y)
+        return fail(ELB_ERR_INVALID_ARG, "NULL tensor pointer");
+    const size_t need = layout(T, d, N, m, params->K, dtype).total;
+    if (need > kScratchBytes)
+        return fail(ELB_ERR_UNSUPPORTED,
+                    "the layer needs %zu bytes of scratch; the allocation-free entry point has "
+                    "%zu (use elb_moe_forward with a workspace)", need, kScratchBytes);
+    void* ws = nullptr;
+    if (int rc = scratch_address(&ws)) return rc;
+    return moe_forward_entry(x, W_router, W_gate_up, W_down, nullptr, residual, T, d, N, m,
+                             dtype, params, y, ws, kScratchBytes, logits_out, k_out, ids_out,
+                             w_out, counts_out, stream);
 }
 
 size_t elb_packed_expert_bytes(int32_t N, int32_t d, int32_t m) {

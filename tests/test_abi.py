@@ -148,3 +148,30 @@ def test_variant_entry_points_validation():
     assert ang(T=0, lg=None) == OK
     # caps up to N are valid for the plain routing now (K = N: the uncapped elbow)
     assert _route(10, 64, K=64, ptr=None) == INVALID            # only the NULL pointers fail
+
+
+def test_noalloc_rejects_oversized_problems_on_the_host():
+    """The allocation-free entry point checks the layer's scratch need against its static
+    array before any HIP call: the OLMoE-shaped layer at T = 8192 needs more than 256 MiB."""
+    lib = B.lib()
+    p = B.RouteParams(8, 1e-8, 0, 0)
+    need = lib.elb_moe_workspace_bytes(8192, 2048, 64, 1024, 8, B.ELB_BF16)
+    assert need > B.NOALLOC_SCRATCH_BYTES
+    assert lib.elb_moe_workspace_bytes(4096, 2048, 64, 1024, 8, B.ELB_BF16) <= \
+        B.NOALLOC_SCRATCH_BYTES
+    rc = lib.elb_moe_forward_noalloc(DUMMY, DUMMY, DUMMY, DUMMY, None, 8192, 2048, 64, 1024,
+                                     B.ELB_BF16, C.byref(p), DUMMY, None, None, None, None,
+                                     None, None)
+    assert rc == UNSUPPORTED
+    assert b"scratch" in lib.elb_last_error()
+    # the other argument checks come first, as in elb_moe_forward
+    bad = B.RouteParams(0, 1e-8, 0, 0)
+    assert lib.elb_moe_forward_noalloc(DUMMY, DUMMY, DUMMY, DUMMY, None, 64, 2048, 64, 1024,
+                                       B.ELB_BF16, C.byref(bad), DUMMY, None, None, None,
+                                       None, None, None) == INVALID
+    assert lib.elb_moe_forward_noalloc(DUMMY, None, DUMMY, DUMMY, None, 64, 2048, 64, 1024,
+                                       B.ELB_BF16, C.byref(p), DUMMY, None, None, None, None,
+                                       None, None) == INVALID
+    assert lib.elb_moe_forward_noalloc(None, None, None, None, None, 0, 2048, 64, 1024,
+                                       B.ELB_BF16, C.byref(p), None, None, None, None, None,
+                                       None, None) == OK
