@@ -34,8 +34,9 @@ def hipcc() -> str:
 FLAGS = ["--offload-arch=" + ARCH, "-O3", "-std=c++17", "-fPIC", "-Wall", "-Wno-inline-asm",
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
          "-I" + os.path.join(ROOT, "include")]
-# Per-file additions (none at present).
-FILE_FLAGS: dict = {}
+# Per-file additions.  route.hip: the routing kernels take finite (or -inf) logits, and
+# without NaN semantics a float min/max on a raw logit needs no canonicalising instruction.
+FILE_FLAGS: dict = {"route.hip": ["-fno-honor-nans"]}
 
 
 def _compile(src: str) -> str:

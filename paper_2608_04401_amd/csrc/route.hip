@@ -8,9 +8,10 @@
 //    two parts of N / 2 columns each (whole 128-byte lines of every row), issued at once;
 //    each lane sorts its row's first half as soon as it has landed (the sorting network run
 //    in part order, sortnet.h PhasedNet) while the second is still in flight.  The tile is
-//    swizzled so that 16 lanes reading their own rows hit 16 distinct bank groups.  The
-//    outputs (k, ids, w) are staged in the tile and stored with whole-wave contiguous
-//    16-byte stores.
+//    swizzled so that 16 lanes reading their own rows hit 16 distinct bank groups.  Each
+//    lane stages its k, ids and w in its own row of the tile and stores them itself (16-byte
+//    stores when K is the template cap).  This file is built without NaN semantics (the
+//    inputs are finite or -inf), so the raw logits are sort keys as they are.
 //  - route_kernel (any N <= 64): the rows staged through registers into a padded LDS tile;
 //    every lane routes its token from its row and stores its own outputs.
 //  - route_x16_kernel (N = 64, batches of at most kSmallBatch tokens): 16 lanes per token
@@ -84,10 +85,10 @@ __device__ __forceinline__ void load_sort_part(const float* tile, int lane, floa
         const float4 v = *reinterpret_cast<const float4*>(
             tile + ((G * 64 * L::CP + lane * L::CP + (cc ^ L::swz(lane))) << 2));
         const int c0 = G * L::B + cc * 4;
-        okey[c0 + 0] = order_key(v.x);
-        okey[c0 + 1] = order_key(v.y);
-        okey[c0 + 2] = order_key(v.z);
-        okey[c0 + 3] = order_key(v.w);
+        okey[c0 + 0] = v.x;  // raw logits: this file is built without NaN semantics, so
+        okey[c0 + 1] = v.y;  // min/max need no canonicalisation, and -0 / +0 compare and
+        okey[c0 + 2] = v.z;  // subtract as equals, so the order and every value derived
+        okey[c0 + 3] = v.w;  // from the keys are those of the canonical keys
 #pragma unroll
         for (int q = 0; q < 4; ++q) key[c0 + q] = okey[c0 + q];
     }
@@ -154,48 +155,38 @@ __global__ __launch_bounds__(256) void route_dma_kernel(const float* __restrict_
     const int k = sorted_elbow<NP, true, KMAX>(key, NP, K, eps, mode, xt, u, S);
     if (lane < rows) kout[t0 + lane] = k;
 
-    // ---- select; outputs staged in the tile (every read of it precedes, in program order,
-    // every write below, and a wave's LDS operations complete in order) ----
+    // ---- select; each lane's outputs staged in its own row of the tile (row stride K + 1
+    // words, odd, so the 64 rows fall in distinct banks), then stored by the lane itself.
+    // Every read of the tile precedes, in program order, every write below, and a wave's LDS
+    // operations complete in order. ----
     int* const stg_i = reinterpret_cast<int*>(tile);
     float* const stg_w = tile + 64 * (KMAX + 1);
     const int ld = K + 1;
     select_emit<NP, true, KMAX>(
-        key, okey, [&](int c) { return order_key(tile[L::at(lane, c)]); }, NP, K, k, u, S,
-        renorm, [&](int j, int id, float w) {
+        key, [&](int c) { return okey[c]; },
+        [&](int c) { return order_key(tile[L::at(lane, c)]); }, NP, K, k, u, S, renorm,
+        [&](int j, int id, float w) {
             stg_i[lane * ld + j] = id;
             stg_w[lane * ld + j] = w;
         });
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-
-    // ---- store the wave's rows * K ids and weights: lane l takes elements 4 l .. 4 l + 3 of
-    // every 256 (one contiguous KB per store instruction) ----
-    const int total = rows * K;
-    int* const gi = ids + t0 * K;
-    float* const gw = wout + t0 * K;
-    for (int e0 = 4 * lane; e0 < total; e0 += 256) {
-        int vi[4];
-        float vw[4];
+    if (lane >= rows) return;
+    int* const gi = ids + (t0 + lane) * K;
+    float* const gw = wout + (t0 + lane) * K;
+    if (vst && K == KMAX) {  // rows of KMAX values, 16-byte aligned: KMAX / 4 stores each
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            const int e = e0 + q < total ? e0 + q : total - 1;
-            // element e is slot j of token tok (K == KMAX: a shift, not a division)
-            const int tok = (K == KMAX) ? e / KMAX : e / K;
-            const int j = e - tok * K;
-            vi[q] = stg_i[tok * ld + j];
-            vw[q] = stg_w[tok * ld + j];
+        for (int q = 0; q < KMAX; q += 4) {
+            const int* si = stg_i + lane * ld + q;
+            const float* sw = stg_w + lane * ld + q;
+            *reinterpret_cast<int4*>(gi + q) = make_int4(si[0], si[1], si[2], si[3]);
+            *reinterpret_cast<float4*>(gw + q) = make_float4(sw[0], sw[1], sw[2], sw[3]);
         }
-        if (vst && e0 + 4 <= total) {
-            *reinterpret_cast<int4*>(gi + e0) = make_int4(vi[0], vi[1], vi[2], vi[3]);
-            *reinterpret_cast<float4*>(gw + e0) = make_float4(vw[0], vw[1], vw[2], vw[3]);
-        } else {
-#pragma unroll
-            for (int q = 0; q < 4; ++q)
-                if (e0 + q < total) {
-                    gi[e0 + q] = vi[q];
-                    gw[e0 + q] = vw[q];
-                }
+    } else {
+        for (int j = 0; j < K; ++j) {
+            gi[j] = stg_i[lane * ld + j];
+            gw[j] = stg_w[lane * ld + j];
         }
     }
 }

@@ -61,11 +61,9 @@ __device__ __forceinline__ void sort_desc(float* key, std::integer_sequence<int,
     (compare_exchange<NP, Q>(key), ...);
 }
 
-// lowest set bit of a 64-bit mask held as two 32-bit halves (0 if empty)
-__device__ __forceinline__ int lowest_bit(uint32_t lo, uint32_t hi) {
-    if (lo) return __builtin_ctz(lo);
-    if (hi) return 32 + __builtin_ctz(hi);
-    return 0;
+// index of the lowest set bit of m | 2^top (m's lowest bit if it has one below top, else top)
+__device__ __forceinline__ int lowest_bit_or(uint64_t m, int top) {
+    return __builtin_ctzll(m | (1ull << top));
 }
 
 // x'_i = i / (N - 1), correctly rounded; +inf past N (pads never win the argmax)
@@ -160,78 +158,84 @@ __device__ __forceinline__ int sorted_elbow(const float (&key)[NP], int Nn, int 
     return k;
 }
 
+// The experts of the first k ranks of the sorted order (keys descending, equal keys by lower
+// expert id), from the sorted keys: tau = the key at rank k - 1; every expert whose key is
+// above tau, then the experts whose key equals tau, lowest ids first.  okey(c): expert c's
+// key (c a compile-time constant).  Returns them as a 64-bit mask over expert ids.  Shared by
+// every kernel that selects from sorted keys alone.
+template <int NP, int KM, class OKey>
+__device__ __forceinline__ uint64_t select_first_k(const float (&key)[NP], OKey&& okey,
+                                                   int Nn, int k) {
+    float tau = key[0];
+#pragma unroll
+    for (int i = 0; i < KM; ++i)
+        if (i == k - 1) tau = key[i];
+    // common case: exactly k experts have a key >= tau (no tie at the boundary)
+    uint64_t sel = 0;
+#pragma unroll
+    for (int c = 0; c < NP; ++c)
+        if (c < Nn && okey(c) >= tau) sel |= 1ull << c;
+    const bool tie = __popcll(sel) != k;
+    if (__builtin_expect(__any(tie), 0)) {  // wave-uniform slow path: ties at tau
+        int g = 0;  // ranks < k with a key above tau
+#pragma unroll
+        for (int i = 0; i < KM; ++i)
+            if (i < k && key[i] > tau) ++g;
+        uint64_t eq = 0;
+        sel = 0;
+#pragma unroll
+        for (int c = 0; c < NP; ++c) {
+            const bool real = c < Nn;
+            if (real && okey(c) > tau) sel |= 1ull << c;
+            if (real && okey(c) == tau) eq |= 1ull << c;
+        }
+        for (int r = 0; r < k - g; ++r) {
+            const uint64_t low = eq & (~eq + 1);  // lowest set bit
+            sel |= low;
+            eq ^= low;
+        }
+    }
+    return sel;
+}
+
+// The k selected experts (select_first_k) in increasing id order, with their keys: cid[r],
+// ck[r] for r < k; ck = -inf (and cid a valid id) for k <= r < KM.  key_of(c): expert c's key
+// re-read from memory (c is not a compile-time constant there).
+template <int NP, int KM, class KeyOf>
+__device__ __forceinline__ void selected_in_id_order(uint64_t sel, KeyOf&& key_of, int k,
+                                                     int (&cid)[KM], float (&ck)[KM]) {
+#pragma unroll
+    for (int r = 0; r < KM; ++r) {
+        const int b = lowest_bit_or(sel, NP - 1);  // r >= k: no bit left, a valid id
+        const float kb = key_of(b);                // read on every lane: no branch
+        cid[r] = b;
+        ck[r] = r < k ? kb : -INFINITY;
+        sel &= sel - 1;
+    }
+}
+
 // The k selected experts (the k largest keys, equal keys by lower id) with their weights,
 // handed to emit(rank, id, w) in no particular order of rank, then emit(j, -1, 0) for
-// k <= j < K.  okey: the token's keys by expert id; key_of(c): expert c's key re-read from
-// memory (c is not a compile-time constant there).
-template <int NP, bool FULL, int KMAX, class KeyOf, class Emit>
-__device__ __forceinline__ void select_emit(const float (&key)[NP], const float (&okey)[NP],
+// k <= j < K.  okey(c): expert c's key (c a compile-time constant); key_of(c): expert c's key
+// re-read from memory (c is not a compile-time constant there).
+template <int NP, bool FULL, int KMAX, class OKey, class KeyOf, class Emit>
+__device__ __forceinline__ void select_emit(const float (&key)[NP], OKey&& okey,
                                             KeyOf&& key_of, int Nn, int K, int k,
                                             const float (&u)[NP], float S, int renorm,
                                             Emit&& emit) {
     constexpr int KM = NP < KMAX ? NP : KMAX;
     const float lmax = key[0];
-    // tau = key of rank k-1; g = ranks < k with a key above tau; the rest of the k come
-    // from the experts whose key equals tau, lowest ids first.
-    float tau = key[0];
-    int g = 0;
-#pragma unroll
-    for (int i = 0; i < KM; ++i)
-        if (i == k - 1) tau = key[i];
-#pragma unroll
-    for (int i = 0; i < KM; ++i)
-        if (i < k && key[i] > tau) ++g;
-    // common case: exactly k experts have a key >= tau (no tie at the boundary)
-    uint32_t sel_lo = 0, sel_hi = 0;
-#pragma unroll
-    for (int c = 0; c < NP; ++c) {
-        const uint32_t bit = (c < Nn && okey[c] >= tau) ? (1u << (c & 31)) : 0u;
-        if (c < 32) sel_lo |= bit;
-        else sel_hi |= bit;
-    }
-    const bool tie = (__popc(sel_lo) + __popc(sel_hi)) != k;
-    if (__any(tie)) {  // wave-uniform slow path: ties at tau, lowest ids first
-        uint32_t eq_lo = 0, eq_hi = 0;
-        sel_lo = sel_hi = 0;
-#pragma unroll
-        for (int c = 0; c < NP; ++c) {
-            const uint32_t bit = 1u << (c & 31);
-            const bool real = c < Nn;
-            const uint32_t gt = (real && okey[c] > tau) ? bit : 0u;
-            const uint32_t eq = (real && okey[c] == tau) ? bit : 0u;
-            if (c < 32) {
-                sel_lo |= gt;
-                eq_lo |= eq;
-            } else {
-                sel_hi |= gt;
-                eq_hi |= eq;
-            }
-        }
-        for (int r = 0; r < k - g; ++r) {
-            const int b = lowest_bit(eq_lo, eq_hi);
-            if (b < 32) { sel_lo |= 1u << b; eq_lo &= ~(1u << b); }
-            else { sel_hi |= 1u << (b - 32); eq_hi &= ~(1u << (b - 32)); }
-        }
-    }
-    // the selected experts in id order, with their keys
+    const uint64_t sel = select_first_k<NP, KM>(key, okey, Nn, k);
     int cid[KM];
     float ck[KM];
-#pragma unroll
-    for (int r = 0; r < KM; ++r) {
-        const int b = lowest_bit(sel_lo, sel_hi);
-        const bool on = r < k;
-        cid[r] = b;
-        ck[r] = on ? key_of(b) : -INFINITY;
-        if (b < 32) sel_lo &= sel_lo - 1;
-        else sel_hi &= sel_hi - 1;
-    }
+    selected_in_id_order<NP, KM>(sel, key_of, k, cid, ck);
     float denom = S;
     if (renorm) {
-        float sel = 0.f;
+        float sl = 0.f;
 #pragma unroll
         for (int j = 0; j < KM; ++j)
-            if (j < k) sel += u[j];
-        denom = sel;
+            if (j < k) sl += u[j];
+        denom = sl;
     }
     const float inv = 1.0f / denom;
     // rank of each in descending order (equal keys: lower id, i.e. lower r, first)
@@ -272,7 +276,8 @@ __device__ __forceinline__ void route_token(const float* row, int N, int K, floa
     const int k = sorted_elbow<NP, FULL, KMAX>(key, Nn, K, eps, mode, xt, u, S);
     kout[t] = k;
     select_emit<NP, FULL, KMAX>(
-        key, okey, [&](int c) { return order_key(row[c]); }, Nn, K, k, u, S, renorm,
+        key, [&](int c) { return okey[c]; }, [&](int c) { return order_key(row[c]); }, Nn, K,
+        k, u, S, renorm,
         [&](int j, int id, float w) {
             ids[t * K + j] = id;
             wout[t * K + j] = w;

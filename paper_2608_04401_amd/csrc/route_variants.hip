@@ -44,62 +44,16 @@ __device__ __forceinline__ void sort_pairs_desc(int64_t* v, std::integer_sequenc
 }
 
 // The experts of the first k ranks from the sorted keys, by the routing kernel's rule
-// (tau = the key at rank k - 1; every key above tau, then keys equal to tau by lowest id):
-// their mask `taken`, and up to KM of them in id order (cid) with their keys (ck, -inf past k;
-// re-read from the token's LDS row, as the id is not a compile-time constant there).
+// (select_first_k): their mask `taken`, and up to KM of them in id order (cid) with their keys
+// (ck, -inf past k; re-read from the token's LDS row, as the id is not a compile-time
+// constant there).
 template <int NP, int KM>
 __device__ __forceinline__ void first_k_experts(const float (&key)[NP], const float (&okey)[NP],
                                                 const float* row, int Nn, int k,
                                                 uint64_t& taken, int (&cid)[KM],
                                                 float (&ck)[KM]) {
-    float tau = key[0];
-#pragma unroll
-    for (int i = 0; i < KM; ++i)
-        if (i == k - 1) tau = key[i];
-    int g = 0;
-#pragma unroll
-    for (int i = 0; i < KM; ++i)
-        if (i < k && key[i] > tau) ++g;
-    uint32_t sel_lo = 0, sel_hi = 0;
-#pragma unroll
-    for (int c = 0; c < NP; ++c) {
-        const uint32_t bit = (c < Nn && okey[c] >= tau) ? (1u << (c & 31)) : 0u;
-        if (c < 32) sel_lo |= bit;
-        else sel_hi |= bit;
-    }
-    const bool tie = (__popc(sel_lo) + __popc(sel_hi)) != k;
-    if (__any(tie)) {  // wave-uniform slow path: ties at tau, lowest ids first
-        uint32_t eq_lo = 0, eq_hi = 0;
-        sel_lo = sel_hi = 0;
-#pragma unroll
-        for (int c = 0; c < NP; ++c) {
-            const uint32_t bit = 1u << (c & 31);
-            const bool real = c < Nn;
-            const uint32_t gt = (real && okey[c] > tau) ? bit : 0u;
-            const uint32_t eq = (real && okey[c] == tau) ? bit : 0u;
-            if (c < 32) {
-                sel_lo |= gt;
-                eq_lo |= eq;
-            } else {
-                sel_hi |= gt;
-                eq_hi |= eq;
-            }
-        }
-        for (int r = 0; r < k - g; ++r) {
-            const int b = lowest_bit(eq_lo, eq_hi);
-            if (b < 32) { sel_lo |= 1u << b; eq_lo &= ~(1u << b); }
-            else { sel_hi |= 1u << (b - 32); eq_hi &= ~(1u << (b - 32)); }
-        }
-    }
-    taken = ((uint64_t)sel_hi << 32) | sel_lo;
-#pragma unroll
-    for (int r = 0; r < KM; ++r) {
-        const int b = lowest_bit(sel_lo, sel_hi);
-        cid[r] = b;
-        ck[r] = r < k ? order_key(row[b]) : -INFINITY;
-        if (b < 32) sel_lo &= sel_lo - 1;
-        else sel_hi &= sel_hi - 1;
-    }
+    taken = select_first_k<NP, KM>(key, [&](int c) { return okey[c]; }, Nn, k);
+    selected_in_id_order<NP, KM>(taken, [&](int c) { return order_key(row[c]); }, k, cid, ck);
 }
 
 // PAIRS: sort (key, id) pairs (a selection with any cap is asked for).  Otherwise the keys
