@@ -38,7 +38,7 @@ inline size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
 // Sub-buffers carved from the caller's workspace, in this order.
 struct Layout {
     size_t hist, tile_off, counts, offsets, row_token, inv, H, Y;  // expert part
-    size_t logits, k, ids, w;                                      // routing (forward only)
+    size_t logits, k, ids, w, part;                                // routing (forward only)
     size_t experts_end, total;
 };
 
@@ -66,6 +66,7 @@ Layout layout(int64_t T, int d, int N, int m, int K, int dtype) {
     L.k = take((size_t)T * 4);
     L.ids = take(rows * 4);
     L.w = take(rows * 4);
+    L.part = take((size_t)4 * T * N * 4);  // the split router's partial logits
     L.total = o;
     return L;
 }
@@ -163,12 +164,16 @@ int scratch_address(void** out) {
 // ---- per-kernel timing ----
 struct Rec {
     const char* name;
+    int scope;  // the ProfileScope instance (a scope may make several launches)
     hipEvent_t a, b;
 };
 std::atomic<bool> g_prof_on{false};
+std::atomic<int> g_scope_seq{0};
 std::mutex g_prof_mu;
 std::vector<Rec> g_recs;
 std::vector<hipEvent_t> g_pool;
+thread_local const char* t_scope_name = nullptr;
+thread_local int t_scope_id = 0;
 
 hipEvent_t pool_get() {
     if (!g_pool.empty()) {
@@ -177,7 +182,7 @@ hipEvent_t pool_get() {
         return e;
     }
     // timing only: without the system-scope fence an event does not write back and
-    // invalidate the caches, which would slow the kernel that follows it
+    // invalidate the caches
     hipEvent_t e = nullptr;
     if (hipEventCreateWithFlags(&e, hipEventDisableSystemFence) != hipSuccess) return nullptr;
     return e;
@@ -185,20 +190,34 @@ hipEvent_t pool_get() {
 
 }  // namespace
 
-ProfileScope::ProfileScope(const char* name, hipStream_t s) : name_(name), s_(s), slot_(-1) {
-    if (!g_prof_on.load(std::memory_order_relaxed)) return;
-    std::lock_guard<std::mutex> lk(g_prof_mu);
-    Rec r{name, pool_get(), pool_get()};
-    if (!r.a || !r.b) return;
-    (void)hipEventRecord(r.a, s);
-    g_recs.push_back(r);
-    slot_ = (int)g_recs.size() - 1;
+ProfileScope::ProfileScope(const char* name, hipStream_t) : prev_name_(t_scope_name),
+                                                            prev_id_(t_scope_id) {
+    if (g_prof_on.load(std::memory_order_relaxed)) {
+        t_scope_name = name;
+        t_scope_id = ++g_scope_seq;
+    } else {
+        t_scope_name = nullptr;
+    }
 }
 
 ProfileScope::~ProfileScope() {
-    if (slot_ < 0) return;
+    t_scope_name = prev_name_;
+    t_scope_id = prev_id_;
+}
+
+bool profile_events(hipEvent_t* start, hipEvent_t* stop) {
+    if (!t_scope_name || !g_prof_on.load(std::memory_order_relaxed)) return false;
     std::lock_guard<std::mutex> lk(g_prof_mu);
-    if (slot_ < (int)g_recs.size()) (void)hipEventRecord(g_recs[slot_].b, s_);
+    Rec r{t_scope_name, t_scope_id, pool_get(), pool_get()};
+    if (!r.a || !r.b) {
+        if (r.a) g_pool.push_back(r.a);
+        if (r.b) g_pool.push_back(r.b);
+        return false;
+    }
+    g_recs.push_back(r);
+    *start = r.a;
+    *stop = r.b;
+    return true;
 }
 
 }  // namespace elb
@@ -342,7 +361,7 @@ static int experts_impl(const void* x, const void* W_gate_up, const void* W_down
                         const int32_t* k, const int32_t* ids, const float* w,
                         const void* residual, int64_t T, int d, int N, int m, int K, int dtype,
                         void* y, char* ws, const Layout& L, int32_t* counts_out,
-                        hipStream_t s) {
+                        hipStream_t s, bool hist_ready = false) {
     int* hist = (int*)(ws + L.hist);
     int* tile_off = (int*)(ws + L.tile_off);
     int* counts = counts_out ? counts_out : (int*)(ws + L.counts);
@@ -370,7 +389,8 @@ static int experts_impl(const void* x, const void* W_gate_up, const void* W_down
                           "combine");
     }
     if (int rc = hip_status(launch_dispatch(k, ids, T, N, K, counts, offsets, row_token, inv,
-                                            hist, tile_off, tail_list, plan, s), "dispatch"))
+                                            hist, tile_off, tail_list, plan, s, hist_ready),
+                            "dispatch"))
         return rc;
     {
         if (int rc = hip_status(launch_gemm_gate_up(x, W_gate_up, row_token, offsets, tile_off,
@@ -449,8 +469,22 @@ static int moe_forward_entry(const void* x, const void* W_router, const void* W_
     int* k = k_out ? k_out : (int*)(ws + L.k);
     int* ids = ids_out ? ids_out : (int*)(ws + L.ids);
     float* w = w_out ? w_out : (float*)(ws + L.w);
-    // small batches with N = 64: the expert-split router and the 16-lane routing (two short
-    // launches) beat the fused kernel, whose blocks each read all of W_r; same bits either way
+    // Router and routing, by size (the same bits on every path): large batches with N = 64
+    // and d % 256 == 0 split the contraction over four blocks per 64 tokens (two launches; the
+    // second also writes the dispatch histogram); small batches with N = 64 use the
+    // expert-split router and the 16-lane routing; the rest the fused one-block kernel, or the
+    // router and routing kernels for fp32 and caps above 16.
+    const bool skinny = gemm_use_skinny(dtype, T, K, N, d, m);
+    if (router_split_usable(dtype, T, d, N, K) && !skinny) {
+        if (int rc = hip_status(
+                launch_router_split_route(x, W_router, T, d, *params, (float*)(ws + L.part),
+                                          logits_out, k, ids, w, (int*)(ws + L.hist),
+                                          dispatch_hist_ld(T), s),
+                "router_split_route"))
+            return rc;
+        return experts_impl(x, W_gate_up, W_down, packed, k, ids, w, residual, T, d, N, m, K,
+                            dtype, y, ws, L, counts_out, s, true);
+    }
     if (router_route_fusable(dtype, K) && !(N == 64 && T <= kSmallBatch)) {
         if (int rc = hip_status(launch_router_route(x, W_router, T, d, N, *params, logits_out,
                                                     k, ids, w, s), "router_route"))
@@ -552,6 +586,8 @@ int elb_profile_enable(int on) {
 int elb_profile_read(const char** names, double* total_ms, int64_t* launches, int cap) {
     std::lock_guard<std::mutex> lk(g_prof_mu);
     std::map<std::string, std::pair<double, int64_t>> acc;
+    std::map<std::string, int> last_scope;
+    std::vector<const char*> order;  // names in first-seen order (static strings)
     int rc = ELB_OK;
     for (Rec& r : g_recs) {
         float ms = 0.f;
@@ -561,21 +597,22 @@ int elb_profile_read(const char** names, double* total_ms, int64_t* launches, in
         auto it = acc.find(r.name);
         if (it == acc.end()) {
             acc[r.name] = {ms, 1};
+            last_scope[r.name] = r.scope;
+            order.push_back(r.name);
         } else {
             it->second.first += ms;
-            it->second.second += 1;
+            if (last_scope[r.name] != r.scope) {  // a new scope instance: one more launch
+                it->second.second += 1;
+                last_scope[r.name] = r.scope;
+            }
         }
         g_pool.push_back(r.a);
         g_pool.push_back(r.b);
     }
-    std::vector<const char*> static_names;
-    for (Rec& r : g_recs)
-        if (std::find(static_names.begin(), static_names.end(), r.name) == static_names.end())
-            static_names.push_back(r.name);
     g_recs.clear();
     if (rc != ELB_OK) return -fail(rc, "profile events failed");
     int n = 0;
-    for (const char* nm : static_names) {
+    for (const char* nm : order) {
         if (n < cap) {
             if (names) names[n] = nm;
             if (total_ms) total_ms[n] = acc[nm].first;

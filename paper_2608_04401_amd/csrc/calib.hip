@@ -44,7 +44,7 @@ __global__ __launch_bounds__(256) void mfma_loop(int iters, float* __restrict__ 
 
 hipError_t launch_calibrate_mfma(int blocks, int iters, float* out, hipStream_t s) {
     ProfileScope prof("calibrate_mfma", s);
-    hipLaunchKernelGGL(mfma_loop, dim3((unsigned)blocks), dim3(256), 0, s, iters, out);
+    ELB_LAUNCH(mfma_loop, dim3((unsigned)blocks), dim3(256), 0, s, iters, out);
     return hipGetLastError();
 }
 

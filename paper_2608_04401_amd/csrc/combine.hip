@@ -80,11 +80,11 @@ hipError_t launch_combine(const void* Y, const int* k, const int* inv, const flo
     if (T == 0) return hipSuccess;
     if (dtype == ELB_BF16) {
         ProfileScope prof("combine_bf16", s);
-        hipLaunchKernelGGL(combine_bf16, dim3((unsigned)T), dim3(256), 0, s, (const bf16_t*)Y, k,
+        ELB_LAUNCH(combine_bf16, dim3((unsigned)T), dim3(256), 0, s, (const bf16_t*)Y, k,
                            inv, w, (const bf16_t*)residual, T, d, K, (bf16_t*)y);
     } else {
         ProfileScope prof("combine_f32", s);
-        hipLaunchKernelGGL(combine_f32, dim3((unsigned)T), dim3(256), 0, s, (const float*)Y, k,
+        ELB_LAUNCH(combine_f32, dim3((unsigned)T), dim3(256), 0, s, (const float*)Y, k,
                            inv, w, (const float*)residual, T, d, K, (float*)y);
     }
     return hipGetLastError();

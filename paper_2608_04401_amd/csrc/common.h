@@ -1,6 +1,7 @@
 // Internal declarations shared by the HIP sources of libelbow_moe (not part of the ABI).
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -72,9 +73,12 @@ constexpr int kTailRows = 32;  // largest remainder the tail kernel takes
 
 // hist: dispatch_hist_ints(T, N) int32 scratch ([N, dispatch_hist_ld(T)], expert-major);
 // tile_off [N + 1]; tail_list [kTailMax + 1]
+// hist_ready: hist already holds the per-group counts (written by the split router), so the
+// count launch is skipped
 hipError_t launch_dispatch(const int* k, const int* ids, int64_t T, int N, int K, int* counts,
                            int* offsets, int* row_token, int* inv, int* hist, int* tile_off,
-                           int* tail_list, const TilePlan& plan, hipStream_t s);
+                           int* tail_list, const TilePlan& plan, hipStream_t s,
+                           bool hist_ready = false);
 
 // router logits
 hipError_t launch_router(const void* x, const void* Wr, int64_t T, int d, int N, int dtype,
@@ -85,6 +89,17 @@ bool router_route_fusable(int dtype, int K);
 hipError_t launch_router_route(const void* x, const void* Wr, int64_t T, int d, int N,
                                const elb_route_params& p, float* logits, int* k, int* ids,
                                float* w, hipStream_t s);
+
+// the layer's router and routing for large batches in two launches (N == 64, bf16, K <=
+// kLaneMaxK, T > kSmallBatch, d % 256 == 0): partial logits per quarter of the contraction
+// into part [4, T, 64] (workspace), then their sum and the routing; also writes the dispatch
+// histogram (hist [64, hist_ld], column g = tokens [64 g, 64 g + 64)).  Same bits as the other
+// router paths.
+bool router_split_usable(int dtype, int64_t T, int d, int N, int K);
+hipError_t launch_router_split_route(const void* x, const void* Wr, int64_t T, int d,
+                                     const elb_route_params& p, float* part, float* logits,
+                                     int* k, int* ids, float* w, int* hist, int64_t hist_ld,
+                                     hipStream_t s);
 
 // grouped GEMMs
 // rows per M-tile of the grouped GEMMs for this problem (the dispatch scan uses the same)
@@ -121,12 +136,27 @@ hipError_t launch_combine(const void* Y, const int* k, const int* inv, const flo
 hipError_t launch_calibrate_mfma(int blocks, int iters, float* out, hipStream_t s);
 
 // ---- per-kernel timing hooks (api.hip) ----
+// A ProfileScope names the launches made while it is alive (on the calling thread).  With the
+// library's profiling on, every ELB_LAUNCH inside a scope carries a start and a stop event in
+// its own dispatch (hipExtLaunchKernelGGL), so timing adds no packets, and no idle gaps,
+// between kernels; with profiling off it is a plain launch.
 struct ProfileScope {
     ProfileScope(const char* name, hipStream_t s);
     ~ProfileScope();
-    const char* name_;
-    hipStream_t s_;
-    int slot_;
+    const char* prev_name_;
+    int prev_id_;
 };
+// events for the next launch of the current scope (false: profiling off or no scope)
+bool profile_events(hipEvent_t* start, hipEvent_t* stop);
+
+#define ELB_LAUNCH(kernel, grid, block, shmem, stream, ...)                                   \
+    do {                                                                                      \
+        hipEvent_t elb_e0_ = nullptr, elb_e1_ = nullptr;                                       \
+        if (::elb::profile_events(&elb_e0_, &elb_e1_))                                         \
+            hipExtLaunchKernelGGL(kernel, grid, block, shmem, stream, elb_e0_, elb_e1_, 0,     \
+                                  __VA_ARGS__);                                               \
+        else                                                                                  \
+            hipLaunchKernelGGL(kernel, grid, block, shmem, stream, __VA_ARGS__);              \
+    } while (0)
 
 }  // namespace elb

@@ -340,10 +340,11 @@ __global__ __launch_bounds__(256) void dispatch_small(const int* __restrict__ k,
 
 hipError_t launch_dispatch(const int* k, const int* ids, int64_t T, int N, int K, int* counts,
                            int* offsets, int* row_token, int* inv, int* hist, int* tile_off,
-                           int* tail_list, const TilePlan& plan, hipStream_t s) {
-    if (T <= 256) {
+                           int* tail_list, const TilePlan& plan, hipStream_t s,
+                           bool hist_ready) {
+    if (T <= 256 && !hist_ready) {
         ProfileScope prof("dispatch_small", s);
-        hipLaunchKernelGGL(dispatch_small, dim3(1), dim3(256), 0, s, k, ids, (int)T, N, K,
+        ELB_LAUNCH(dispatch_small, dim3(1), dim3(256), 0, s, k, ids, (int)T, N, K,
                            counts, offsets, tile_off, tail_list, plan, row_token, inv);
         return hipGetLastError();
     }
@@ -353,25 +354,24 @@ hipError_t launch_dispatch(const int* k, const int* ids, int64_t T, int N, int K
     // at least one scatter block, which also writes offsets and tile_off (also when T == 0)
     const int64_t nb = (groups + kDispWaves - 1) / kDispWaves;
     const unsigned blocks = (unsigned)(nb > 0 ? nb : 1);
-    {
+    if (T > 0 && !hist_ready) {
         ProfileScope prof("dispatch_count", s);
-        if (T > 0)
-            hipLaunchKernelGGL(dispatch_count, dim3(blocks), dim3(64 * kDispWaves), 0, s, k,
-                               ids, T, N, K, ld, hist);
+        ELB_LAUNCH(dispatch_count, dim3(blocks), dim3(64 * kDispWaves), 0, s, k, ids, T,
+                           N, K, ld, hist);
     }
     if (!direct) {
         ProfileScope prof("dispatch_scan", s);
-        hipLaunchKernelGGL(dispatch_scan, dim3((unsigned)N), dim3(1024), 0, s, hist, groups, ld,
+        ELB_LAUNCH(dispatch_scan, dim3((unsigned)N), dim3(1024), 0, s, hist, groups, ld,
                            counts);
     }
     {
         ProfileScope prof("dispatch_scatter", s);
         if (direct)
-            hipLaunchKernelGGL(dispatch_scatter<true>, dim3(blocks), dim3(64 * kDispWaves), 0,
+            ELB_LAUNCH(dispatch_scatter<true>, dim3(blocks), dim3(64 * kDispWaves), 0,
                                s, k, ids, T, N, K, ld, hist, counts, offsets, tile_off,
                                tail_list, plan, row_token, inv);
         else
-            hipLaunchKernelGGL(dispatch_scatter<false>, dim3(blocks), dim3(64 * kDispWaves), 0,
+            ELB_LAUNCH(dispatch_scatter<false>, dim3(blocks), dim3(64 * kDispWaves), 0,
                                s, k, ids, T, N, K, ld, hist, counts, offsets, tile_off,
                                tail_list, plan, row_token, inv);
     }

@@ -709,17 +709,17 @@ hipError_t launch_gemm_gate_up(const void* x, const void* Wgu, const int* row_to
         ProfileScope prof("gemm_gate_up_bf16", s);
         const unsigned big = grid8(max_tiles * (m / 128));
         const unsigned tail = tail_list ? (unsigned)(kTailMax * (m / 32)) : 0u;
-        hipLaunchKernelGGL(gemm_bf16_dma<0>, dim3(big + tail), dim3(256), 0, s,
+        ELB_LAUNCH(gemm_bf16_dma<0>, dim3(big + tail), dim3(256), 0, s,
                            (const bf16_t*)x, row_token, (const bf16_t*)Wgu, offsets, tile_off,
                            tail_list, (int)big, N, d, m, (bf16_t*)H);
     } else if (dtype == ELB_BF16) {
         ProfileScope prof("gemm_gate_up_bf16_s", s);
-        hipLaunchKernelGGL(gemm_bf16<0>, dim3(grid8(max_tiles * (m / 64))), dim3(256),
+        ELB_LAUNCH(gemm_bf16<0>, dim3(grid8(max_tiles * (m / 64))), dim3(256),
                            0, s, (const bf16_t*)x, row_token, (const bf16_t*)Wgu, offsets,
                            tile_off, N, d, m, (bf16_t*)H);
     } else {
         ProfileScope prof("gemm_gate_up_f32", s);
-        hipLaunchKernelGGL(gemm_f32<0>, dim3((unsigned)max_tiles, (unsigned)((m + 31) / 32)),
+        ELB_LAUNCH(gemm_f32<0>, dim3((unsigned)max_tiles, (unsigned)((m + 31) / 32)),
                            dim3(256), 0, s, (const float*)x, row_token, (const float*)Wgu,
                            offsets, tile_off, N, d, m, (float*)H);
     }
@@ -735,17 +735,17 @@ hipError_t launch_gemm_down(const void* H, const void* Wd, const int* offsets,
         ProfileScope prof("gemm_down_bf16", s);
         const unsigned big = grid8(max_tiles * ((d + LBN - 1) / LBN));
         const unsigned tail = tail_list ? (unsigned)(kTailMax * (d / 64)) : 0u;
-        hipLaunchKernelGGL(gemm_bf16_dma<1>, dim3(big + tail), dim3(256), 0, s,
+        ELB_LAUNCH(gemm_bf16_dma<1>, dim3(big + tail), dim3(256), 0, s,
                            (const bf16_t*)H, (const int*)nullptr, (const bf16_t*)Wd, offsets,
                            tile_off, tail_list, (int)big, N, d, m, (bf16_t*)Y);
     } else if (dtype == ELB_BF16) {
         ProfileScope prof("gemm_down_bf16_s", s);
-        hipLaunchKernelGGL(gemm_bf16<1>, dim3(grid8(max_tiles * ((d + BN - 1) / BN))),
+        ELB_LAUNCH(gemm_bf16<1>, dim3(grid8(max_tiles * ((d + BN - 1) / BN))),
                            dim3(256), 0, s, (const bf16_t*)H, (const int*)nullptr,
                            (const bf16_t*)Wd, offsets, tile_off, N, d, m, (bf16_t*)Y);
     } else {
         ProfileScope prof("gemm_down_f32", s);
-        hipLaunchKernelGGL(gemm_f32<1>, dim3((unsigned)max_tiles, (unsigned)((d + FBN - 1) / FBN)),
+        ELB_LAUNCH(gemm_f32<1>, dim3((unsigned)max_tiles, (unsigned)((d + FBN - 1) / FBN)),
                            dim3(256), 0, s, (const float*)H, (const int*)nullptr,
                            (const float*)Wd, offsets, tile_off, N, d, m, (float*)Y);
     }

@@ -177,11 +177,11 @@ hipError_t launch_gemm_skinny(const void* x, const void* Wgu, const void* Wd, co
     {
         ProfileScope prof("gemm_gate_up_skinny", s);
         if (pgu)
-            hipLaunchKernelGGL((gemm_skinny<0, true>), dim3(blocks_for(N * (m / 32))), dim3(256),
+            ELB_LAUNCH((gemm_skinny<0, true>), dim3(blocks_for(N * (m / 32))), dim3(256),
                                0, s, (const bf16_t*)x, k, ids, t, K, pgu, N, d, m, (bf16_t*)H,
                                counts);
         else
-            hipLaunchKernelGGL((gemm_skinny<0, false>), dim3(blocks_for(N * (m / 32))),
+            ELB_LAUNCH((gemm_skinny<0, false>), dim3(blocks_for(N * (m / 32))),
                                dim3(256), 0, s, (const bf16_t*)x, k, ids, t, K,
                                (const bf16_t*)Wgu, N, d, m, (bf16_t*)H, counts);
     }
@@ -189,11 +189,11 @@ hipError_t launch_gemm_skinny(const void* x, const void* Wgu, const void* Wd, co
     {
         ProfileScope prof("gemm_down_skinny", s);
         if (pd)
-            hipLaunchKernelGGL((gemm_skinny<1, true>), dim3(blocks_for(N * (d / 64))), dim3(256),
+            ELB_LAUNCH((gemm_skinny<1, true>), dim3(blocks_for(N * (d / 64))), dim3(256),
                                0, s, (const bf16_t*)H, k, ids, t, K, pd, N, d, m, (bf16_t*)Y,
                                (int*)nullptr);
         else
-            hipLaunchKernelGGL((gemm_skinny<1, false>), dim3(blocks_for(N * (d / 64))),
+            ELB_LAUNCH((gemm_skinny<1, false>), dim3(blocks_for(N * (d / 64))),
                                dim3(256), 0, s, (const bf16_t*)H, k, ids, t, K,
                                (const bf16_t*)Wd, N, d, m, (bf16_t*)Y, (int*)nullptr);
     }
@@ -205,7 +205,7 @@ hipError_t launch_pack_experts(const void* Wgu, const void* Wd, int N, int d, in
     const int64_t n_all = ((int64_t)N * 2 * m * d + (int64_t)N * d * m) / 8;
     if (n_all == 0) return hipSuccess;
     ProfileScope prof("pack_experts", s);
-    hipLaunchKernelGGL(pack_experts, dim3((unsigned)((n_all + 255) / 256)), dim3(256), 0, s,
+    ELB_LAUNCH(pack_experts, dim3((unsigned)((n_all + 255) / 256)), dim3(256), 0, s,
                        (const bf16_t*)Wgu, (const bf16_t*)Wd, N, d, m, (bf16_t*)packed);
     return hipGetLastError();
 }

@@ -202,12 +202,12 @@ hipError_t launch_np(const float* logits, int64_t T, int N, const elb_route_para
     if constexpr (FULL && NP >= 16) {
         if (vec4) {
             const int vst = ((uintptr_t)ids % 16) == 0 && ((uintptr_t)w % 16) == 0;
-            hipLaunchKernelGGL((route_dma_kernel<NP, KMAX>), dim3(blocks), dim3(256), 0, s,
+            ELB_LAUNCH((route_dma_kernel<NP, KMAX>), dim3(blocks), dim3(256), 0, s,
                                logits, T, p.K, p.eps, p.mode, p.renormalize, vst, xt, k, ids, w);
             return hipGetLastError();
         }
     }
-    hipLaunchKernelGGL((route_kernel<NP, FULL, KMAX>), dim3(blocks), dim3(256), 0, s, logits, T, N, p.K,
+    ELB_LAUNCH((route_kernel<NP, FULL, KMAX>), dim3(blocks), dim3(256), 0, s, logits, T, N, p.K,
                        p.eps, p.mode, p.renormalize, vec4, xt, k, ids, w);
     return hipGetLastError();
 }
@@ -241,7 +241,7 @@ hipError_t launch_k(const float* logits, int64_t T, int N, const elb_route_param
                    int* ids, float* w, hipStream_t s) {
     if (N == 64 && T <= kSmallBatch) {
         ProfileScope prof("route", s);
-        hipLaunchKernelGGL((route_x16_kernel<KMAX>), dim3((unsigned)((T + 15) / 16)), dim3(256),
+        ELB_LAUNCH((route_x16_kernel<KMAX>), dim3((unsigned)((T + 15) / 16)), dim3(256),
                            0, s, logits, T, p.K, p.eps, p.mode, p.renormalize, make_xtable(N), k,
                            ids, w);
         return hipGetLastError();

@@ -61,6 +61,18 @@ __device__ __forceinline__ void sort_desc(float* key, std::integer_sequence<int,
     (compare_exchange<NP, Q>(key), ...);
 }
 
+// Balanced pairwise sum of v[0..n), n a power of two: ((v0 + v1) + (v2 + v3)) + ...  Every
+// kernel sums S (and a renormalised denominator) over the ranks in this one order, so that
+// all of them give the same bits: a lane that holds all n values adds them in this tree, and
+// lanes holding 4 consecutive ranks each add their 4 as (v0 + v1) + (v2 + v3) and then
+// combine with a butterfly (shfl_xor 1, 2, 4, ...), which walks the same tree (IEEE addition
+// is commutative, and adding the exact zeros of masked ranks changes nothing).
+template <int n>
+__device__ __forceinline__ float tree_sum(const float* v) {
+    if constexpr (n == 1) return v[0];
+    else return tree_sum<n / 2>(v) + tree_sum<n / 2>(v + n / 2);
+}
+
 // index of the lowest set bit of m | 2^top (m's lowest bit if it has one below top, else top)
 __device__ __forceinline__ int lowest_bit_or(uint64_t m, int top) {
     return __builtin_ctzll(m | (1ull << top));
@@ -112,20 +124,17 @@ __device__ __forceinline__ void stage_rows(const float* __restrict__ src, int N,
 
 // ---- the per-token steps, shared by every kernel that routes in one lane ----
 
-// u_i = exp(l_(i) - l_(0)) in rank order (0 for pads), S = sum u in rank order, and the
-// elbow's k (K in top-K mode) from the sorted keys.
+// u_i = exp(l_(i) - l_(0)) in rank order (0 for pads), S = sum u over the ranks (tree_sum),
+// and the elbow's k (K in top-K mode) from the sorted keys.
 template <int NP, bool FULL, int KMAX>
 __device__ __forceinline__ int sorted_elbow(const float (&key)[NP], int Nn, int K, float eps,
                                             int mode, const XTable& xt, float (&u)[NP],
                                             float& S) {
     constexpr int KM = NP < KMAX ? NP : KMAX;
     const float lmax = key[0];
-    S = 0.f;
 #pragma unroll
-    for (int i = 0; i < NP; ++i) {
-        u[i] = __builtin_amdgcn_exp2f((key[i] - lmax) * kLog2e);
-        S += u[i];
-    }
+    for (int i = 0; i < NP; ++i) u[i] = __builtin_amdgcn_exp2f((key[i] - lmax) * kLog2e);
+    S = tree_sum<NP>(u);
     float umin = u[NP - 1];
     if (!FULL) {
 #pragma unroll
@@ -231,11 +240,10 @@ __device__ __forceinline__ void select_emit(const float (&key)[NP], OKey&& okey,
     selected_in_id_order<NP, KM>(sel, key_of, k, cid, ck);
     float denom = S;
     if (renorm) {
-        float sl = 0.f;
+        float sel_u[KM];
 #pragma unroll
-        for (int j = 0; j < KM; ++j)
-            if (j < k) sl += u[j];
-        denom = sl;
+        for (int j = 0; j < KM; ++j) sel_u[j] = j < k ? u[j] : 0.f;
+        denom = tree_sum<KM>(sel_u);
     }
     const float inv = 1.0f / denom;
     // rank of each in descending order (equal keys: lower id, i.e. lower r, first)
@@ -302,14 +310,17 @@ __device__ __forceinline__ int64_t shfl_xor64(int64_t v, int m) {
     return ((int64_t)hi << 32) | (uint32_t)lo;
 }
 
-// row: the token's 64 logits in LDS (overwritten with its u values); every lane of the
-// group calls this (valid: the token exists; only valid groups write)
+// row: the token's 64 logits in LDS; every lane of the group calls this (valid: the token
+// exists; only valid groups write)
+// lds_hist (optional): a 64-bin LDS histogram to which each selected expert of a valid token
+// adds one (the dispatch's per-group counts).
 template <int KMAX>
 __device__ __forceinline__ void route_token_x16(float* row, int K, float eps, int mode,
                                                 int renorm, const XTable& xt, int64_t t,
                                                 bool valid, int* __restrict__ kout,
                                                 int* __restrict__ ids,
-                                                float* __restrict__ wout) {
+                                                float* __restrict__ wout,
+                                                int* lds_hist = nullptr) {
     constexpr int NP = 64;
     const int sl = threadIdx.x & 15;
     // ---- (key, id) pairs of positions 4 sl + i: key image high, 63 - id low ----
@@ -361,19 +372,11 @@ __device__ __forceinline__ void route_token_x16(float* row, int K, float eps, in
     const float lmax = __shfl(key[0], 0, 16);
     float u[4];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        u[i] = __builtin_amdgcn_exp2f((key[i] - lmax) * kLog2e);
-        row[4 * sl + i] = u[i];  // rank order; the group's logits have all been read
-    }
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-    // ---- S in rank order (first lane), u_min = u of rank 63 ----
-    float S = 0.f;
-    if (sl == 0) {
-        for (int i = 0; i < NP; ++i) S += row[i];
-    }
-    S = __shfl(S, 0, 16);
+    for (int i = 0; i < 4; ++i) u[i] = __builtin_amdgcn_exp2f((key[i] - lmax) * kLog2e);
+    // ---- S over the ranks (tree_sum by a butterfly), u_min = u of rank 63 ----
+    float S = (u[0] + u[1]) + (u[2] + u[3]);
+#pragma unroll
+    for (int m = 1; m < 16; m <<= 1) S += __shfl_xor(S, m, 16);
     const float umin = __shfl(u[3], 15, 16);
     int k = K;
     if (mode == ELB_MODE_ELBOW) {
@@ -409,13 +412,13 @@ __device__ __forceinline__ void route_token_x16(float* row, int K, float eps, in
         k = (tail > bd) ? K : be + 1;
     }
     float denom = S;
-    if (renorm) {
-        float sel = 0.f;
-        if (sl == 0) {
-            for (int j = 0; j < KMAX; ++j)
-                if (j < k) sel += row[j];
-        }
-        denom = __shfl(sel, 0, 16);
+    if (renorm) {  // the selected ranks' u, the others as exact zeros, in the same tree
+        float m4[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) m4[i] = (4 * sl + i < k) ? u[i] : 0.f;
+        denom = (m4[0] + m4[1]) + (m4[2] + m4[3]);
+#pragma unroll
+        for (int m = 1; m < 16; m <<= 1) denom += __shfl_xor(denom, m, 16);
     }
     const float inv = 1.0f / denom;
     if (!valid) return;
@@ -427,6 +430,7 @@ __device__ __forceinline__ void route_token_x16(float* row, int K, float eps, in
             ids[t * K + r] = (r < k) ? id[i] : -1;
             wout[t * K + r] = (r < k) ? u[i] * inv : 0.f;
         }
+        if (lds_hist && r < k) atomicAdd(&lds_hist[id[i]], 1);
     }
 }
 

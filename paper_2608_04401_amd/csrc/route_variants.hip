@@ -6,8 +6,8 @@
 // One LANE per token with the routing kernel's staging and arithmetic (route_lane.h), but the
 // sorting network carries the expert ids along with the logits, so the id at every rank is
 // known and any cap up to N costs the same.  Same bits as the routing kernel: the same keys,
-// u_i = exp(l_(i) - l_(0)) in rank order, S summed in rank order, the same scaled deviation
-// and first argmax, w = u * (1 / denominator).  The elbow angle (no selection asked for) and
+// u_i = exp(l_(i) - l_(0)) in rank order, S as the same tree over the ranks (tree_sum), the
+// same scaled deviation and first argmax, w = u * (1 / denominator).  The elbow angle (no selection asked for) and
 // tail randomisation with K <= 16 sort the keys only.
 #include "route_lane.h"
 
@@ -112,12 +112,9 @@ __global__ __launch_bounds__(256) void route_pair_kernel(
     // ---- u, S, u_min and the elbow: the routing kernel's arithmetic, in rank order ----
     const float lmax = key[0];
     float u[NP];
-    float S = 0.f;
 #pragma unroll
-    for (int i = 0; i < NP; ++i) {
-        u[i] = __builtin_amdgcn_exp2f((key[i] - lmax) * kLog2e);
-        S += u[i];
-    }
+    for (int i = 0; i < NP; ++i) u[i] = __builtin_amdgcn_exp2f((key[i] - lmax) * kLog2e);
+    const float S = tree_sum<NP>(u);
     float umin = u[NP - 1];
     if (!FULL) {
 #pragma unroll
@@ -174,10 +171,10 @@ __global__ __launch_bounds__(256) void route_pair_kernel(
         for (int c = 0; c < NP; ++c) draw[c] = (c < Nn) ? rr[c] : INFINITY;
         float denom = S;
         if (renorm) {
-            denom = 0.f;
+            float sel_u[KM];
 #pragma unroll
-            for (int j = 0; j < KM; ++j)
-                if (j < k) denom += u[j];
+            for (int j = 0; j < KM; ++j) sel_u[j] = j < k ? u[j] : 0.f;
+            denom = tree_sum<KM>(sel_u);
         }
         for (int j = k; j < K; ++j) {
             float bv = INFINITY;
@@ -230,10 +227,10 @@ __global__ __launch_bounds__(256) void route_pair_kernel(
 
         float denom = S;
         if (renorm) {
-            denom = 0.f;
+            float sel_u[NP];
 #pragma unroll
-            for (int j = 0; j < NP; ++j)
-                if (j < k) denom += u[j];
+            for (int j = 0; j < NP; ++j) sel_u[j] = j < k ? u[j] : 0.f;
+            denom = tree_sum<NP>(sel_u);
         }
         // pass 1: the tail's ids, with unnormalised weights u (the denominator needs them all)
         for (int j = k; j < K; ++j) {
@@ -267,11 +264,10 @@ __global__ __launch_bounds__(256) void route_pair_kernel(
     }
     float denom = S;
     if (renorm) {
-        float sel = 0.f;
+        float sel_u[NP];
 #pragma unroll
-        for (int j = 0; j < NP; ++j)
-            if (j < k) sel += u[j];
-        denom = sel;
+        for (int j = 0; j < NP; ++j) sel_u[j] = j < k ? u[j] : 0.f;
+        denom = tree_sum<NP>(sel_u);
     }
     const float inv = 1.0f / denom;
     if (K <= 16) {  // few slots: direct stores
@@ -314,11 +310,11 @@ void launch_pair_np(const float* logits, const float* rand, int64_t T, int N,
     // keys only: the elbow angle (no ids), or tail randomisation with K <= kLaneMaxK
     const bool keys_only = !ids || (rand && p.K <= kLaneMaxK);
     if (!keys_only)
-        hipLaunchKernelGGL((route_pair_kernel<NP, FULL, true>), grid, dim3(256), 0, s, logits,
+        ELB_LAUNCH((route_pair_kernel<NP, FULL, true>), grid, dim3(256), 0, s, logits,
                            rand, T, N, p.K, p.eps, p.mode, p.renormalize, vec4, make_xtable(N),
                            k, ids, w, e, theta);
     else
-        hipLaunchKernelGGL((route_pair_kernel<NP, FULL, false>), grid, dim3(256), 0, s, logits,
+        ELB_LAUNCH((route_pair_kernel<NP, FULL, false>), grid, dim3(256), 0, s, logits,
                            rand, T, N, p.K, p.eps, p.mode, p.renormalize, vec4,
                            make_xtable(N), k, ids, w, e, theta);
 }

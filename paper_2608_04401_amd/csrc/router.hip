@@ -1,11 +1,11 @@
 // Router logits l = x W_r^T (Section 2: a learned router produces logits l(x) in R^N),
 // fp32 accumulation and fp32 output; and the router fused with the routing of its logits.
 //
-// bf16: one block of 4 waves per 16 tokens.  The 32-deep k-steps are dealt round-robin to
-// the waves, so each wave reads a distinct quarter of the 16 x d slice of x (x is read once)
-// and the matching columns of all N rows of W_r (which stays in L2 across blocks); each wave
-// runs 4 v_mfma_f32_16x16x32_bf16 chains (16 experts each) with its loads four steps ahead
-// of their use, and the 4 partial 16 x N tiles are summed in LDS in a fixed order.
+// bf16: one block of 4 waves per 16 tokens.  Wave w takes the w-th contiguous quarter of the
+// 32-deep k-steps (router_slice), so it reads a distinct quarter of the 16 x d slice of x (x
+// is read once) and the matching columns of all N rows of W_r (which stays in L2 across
+// blocks); each wave runs 4 v_mfma_f32_16x16x32_bf16 chains (16 experts each) with its loads
+// four steps ahead of their use, and the 4 partial 16 x N tiles are summed in LDS in order.
 // N <= 64, d % 32 == 0.
 // fp32: one thread per (token, expert) dot product (the small fp32 configuration).
 #include "route_lane.h"
@@ -15,6 +15,16 @@ namespace elb {
 namespace {
 
 constexpr int RW = 4;  // waves per router block
+
+// The order in which every router kernel accumulates a logit (so that all of them give the same
+// bits): the d / 32 k-steps of 32 are cut into RW contiguous slices, slice s holding steps
+// [s n / RW, (s + 1) n / RW); each slice is one chain of MFMAs over its steps in order,
+// starting from zero, and the logit is ((P_0 + P_1) + P_2) + P_3 in fp32.
+__device__ __forceinline__ void router_slice(int d, int s, int& first, int& count) {
+    const int n = d / 32;
+    first = s * n / RW;
+    count = (s + 1) * n / RW - first;
+}
 
 // The logits of tokens [t0, t0 + 16) and experts [16 g0, 16 (g0 + NG)) (NG groups of 16):
 // each wave's partial sums over its k-steps go to part[w] (lane rows, expert columns
@@ -41,16 +51,16 @@ __device__ __forceinline__ void router_partials(const bf16_t* __restrict__ x,
     f32x4_t acc[NG];
 #pragma unroll
     for (int g = 0; g < NG; ++g) acc[g] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-    // wave w takes the 32-deep k-steps w, w + RW, w + 2 RW, ... (its steps j = 0, 1, ...).  A
-    // ring of R register slots keeps R - 1 steps in flight: step j lives in slot j % R, and
-    // while step j is multiplied, step j + R - 1 is loaded into the slot step j - 1 has just
-    // freed.  Unrolled by R, so every slot index is a constant.
+    // wave w takes the w-th quarter of the 32-deep k-steps (router_slice), in order.  A ring
+    // of R register slots keeps R - 1 steps in flight: step j lives in slot j % R, and while
+    // step j is multiplied, step j + R - 1 is loaded into the slot step j - 1 has just freed.
+    // Unrolled by R, so every slot index is a constant.
     constexpr int R = 5;
-    const int nsteps = d / 32;
-    const int mine = (nsteps - w + RW - 1) / RW;  // steps of this wave
+    int first, mine;
+    router_slice(d, w, first, mine);
     bf16x8_t ra[R], rb[R][NG];
     auto load = [&](int slot_j, bf16x8_t& a, bf16x8_t (&bb)[NG]) {
-        const int k0 = (slot_j < mine ? w + RW * slot_j : 0) * 32;  // past the end: step 0
+        const int k0 = (slot_j < mine ? first + slot_j : 0) * 32;  // past the end: step 0
         a = *reinterpret_cast<const bf16x8_t*>(ap + k0);
 #pragma unroll
         for (int g = 0; g < NG; ++g) bb[g] = *reinterpret_cast<const bf16x8_t*>(bp[g] + k0);
@@ -154,6 +164,161 @@ __global__ __launch_bounds__(64 * RW) void router_route_bf16(
     }
 }
 
+// ---- split router: the layer's router and routing for large batches (N = 64) ----
+//
+// router_split_bf16: block (64-token group, slice s) computes partial logit P_s of its 64
+// tokens x 64 experts over slice s of the contraction (router_slice), in the same MFMA
+// chains as the one-block kernels, so P_s has the same bits.  Both operands go through LDS:
+// per 64-column chunk, the block copies its 64 x rows and the 64 W_r rows (128 bytes, one
+// cache line, per row) straight into LDS with global_load_lds_dwordx4 (8 rows per
+// instruction, 16-byte chunks XOR-swizzled by row so that the MFMA operand reads of 16
+// consecutive rows spread over the banks), up to seven chunks ahead in a ring of eight (at
+// d = 2048 a slice is eight chunks, all in flight at once).  A block reads
+// 64 KB of x and 64 KB of W_r at d = 2048, instead of the 256 KB of W_r that every 16-token
+// block of the one-block kernel streams.  Wave w multiplies tokens [16 w, 16 w + 16) by all
+// 64 experts.  The partials go to part[s][t][n] (workspace).
+// route_split_sum: block of 64 tokens (16 waves, 16 lanes per token): the four partials
+// summed in order (the logit), then route_token_x16; the block also writes its group's
+// per-expert assignment count (the dispatch histogram column of these 64 tokens).
+// Requires N == 64 and d % 256 == 0 (every slice a whole number of 64-column chunks).
+constexpr int kSplitRing = 8;                // chunks in the ring (128 KB of LDS)
+constexpr int kSplitSlot = 2 * 64 * 128;     // bytes per chunk: 64 W_r rows, then 64 x rows
+
+__global__ __launch_bounds__(256) void router_split_bf16(const bf16_t* __restrict__ x,
+                                                         const bf16_t* __restrict__ Wr,
+                                                         int64_t T, int d,
+                                                         float* __restrict__ part) {
+    __shared__ __attribute__((aligned(1024))) char sm[kSplitRing * kSplitSlot];
+    const int s = blockIdx.y;
+    const int64_t t0 = (int64_t)blockIdx.x * 64;
+    const int lane = threadIdx.x & 63;
+    const int w = threadIdx.x >> 6;
+    int first, steps;
+    router_slice(d, s, first, steps);  // d % 256 == 0: first and steps are even
+    const int c0 = first / 2, nc = steps / 2;
+    const bf16_t* const xb = x + t0 * d;  // the block's first token row
+    // copy sources: wave w copies rows [16 w, 16 w + 16) of W_r and of x, 8 rows (1 KB) per
+    // instruction; lane l fills physical chunk l & 7 of row 16 w + 8 i + (l >> 3), i.e. it
+    // fetches that row's logical chunk (l & 7) ^ (row & 7)
+    uint32_t woff[2], xoff[2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+        const int r = 16 * w + 8 * i + (lane >> 3);
+        const int q = (lane & 7) ^ (r & 7);
+        const int tr = (t0 + r < T) ? r : (int)(T - 1 - t0);  // rows past T: never stored
+        woff[i] = ((uint32_t)r * (uint32_t)d + c0 * 64 + q * 8) * 2u;
+        xoff[i] = ((uint32_t)tr * (uint32_t)d + c0 * 64 + q * 8) * 2u;
+    }
+    const uint32_t lds0 = (uint32_t)(uintptr_t)(lds_void_t*)sm;
+    auto issue = [&](int c, int slot) {  // chunk c of the slice into ring slot `slot`
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+            const uint32_t lw = __builtin_amdgcn_readfirstlane(
+                lds0 + slot * kSplitSlot + (2 * w + i) * 1024);
+            const uint32_t lx = lw + 64 * 128;
+            const uint32_t vw = woff[i] + c * 128, vx = xoff[i] + c * 128;
+            asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2"
+                         :: "s"(lw), "v"(vw), "s"(Wr) : "memory", "m0");
+            asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2"
+                         :: "s"(lx), "v"(vx), "s"(xb) : "memory", "m0");
+        }
+    };
+    f32x4_t acc[4];
+#pragma unroll
+    for (int g = 0; g < 4; ++g) acc[g] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    const int l16 = lane & 15, hq = lane >> 4;
+    const int arow = 16 * w + l16;  // the A operand's row (token) of this lane
+#pragma unroll
+    for (int p = 0; p < kSplitRing - 1; ++p)
+        if (p < nc) issue(p, p);
+    for (int c = 0; c < nc; ++c) {
+        // this wave's copies of chunk c are done when at most those of the chunks issued
+        // after it (at most kSplitRing - 2, four instructions each) are in flight; the barrier
+        // then makes every wave's copies of chunk c visible and frees the slot of chunk c - 1,
+        // whose reads every wave has completed
+        const int left = nc - 1 - c;
+        switch (left < kSplitRing - 2 ? left : kSplitRing - 2) {
+            case 0: ELB_WAIT_VMCNT(0); break;
+            case 1: ELB_WAIT_VMCNT(4); break;
+            case 2: ELB_WAIT_VMCNT(8); break;
+            case 3: ELB_WAIT_VMCNT(12); break;
+            case 4: ELB_WAIT_VMCNT(16); break;
+            case 5: ELB_WAIT_VMCNT(20); break;
+            default: ELB_WAIT_VMCNT(24); break;
+        }
+        asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+        if (c + kSplitRing - 1 < nc) issue(c + kSplitRing - 1, (c + kSplitRing - 1) % kSplitRing);
+        const char* const sl = sm + (c % kSplitRing) * kSplitSlot;
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {  // the chunk's two 32-deep k-steps
+            const int q = 4 * j + hq;  // logical 16-byte chunk of this lane's 8 k values
+            const bf16x8_t a = *reinterpret_cast<const bf16x8_t*>(
+                sl + 64 * 128 + arow * 128 + ((q ^ (arow & 7)) << 4));
+            bf16x8_t b[4];
+#pragma unroll
+            for (int g = 0; g < 4; ++g) {
+                const int n = 16 * g + l16;
+                b[g] = *reinterpret_cast<const bf16x8_t*>(sl + n * 128 + ((q ^ (n & 7)) << 4));
+            }
+#pragma unroll
+            for (int g = 0; g < 4; ++g)
+                acc[g] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b[g], acc[g], 0, 0, 0);
+        }
+    }
+    // lane: tokens 16 w + 4 hq + r (r < 4), expert 16 g + l16
+    float* const pp = part + ((int64_t)s * T + t0) * 64;
+#pragma unroll
+    for (int g = 0; g < 4; ++g)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+            const int tr = 16 * w + 4 * hq + r;
+            if (t0 + tr < T) pp[(int64_t)tr * 64 + 16 * g + l16] = acc[g][r];
+        }
+}
+
+template <int KMAX>
+__global__ __launch_bounds__(1024) void route_split_sum(const float* __restrict__ part,
+                                                        int64_t T, int K, float eps, int mode,
+                                                        int renorm, XTable xt,
+                                                        float* __restrict__ logits,
+                                                        int* __restrict__ kout,
+                                                        int* __restrict__ ids,
+                                                        float* __restrict__ wout,
+                                                        int* __restrict__ hist,
+                                                        int64_t hist_ld) {
+    __shared__ float rows[64][65];
+    __shared__ int h[64];
+    const int64_t t0 = (int64_t)blockIdx.x * 64;
+    const int tr = threadIdx.x >> 4, sl = threadIdx.x & 15;
+    if (threadIdx.x < 64) h[threadIdx.x] = 0;
+    const int64_t t = t0 + tr;
+    const bool valid = t < T;
+    // experts 4 sl .. 4 sl + 3 of token t: ((P_0 + P_1) + P_2) + P_3
+    float v[4] = {0.f, 0.f, 0.f, 0.f};  // rows past T: finite, never stored
+    if (valid) {
+        const int64_t slab = T * 64;
+        const float* p0 = part + t * 64 + 4 * sl;
+        const float4 a = *reinterpret_cast<const float4*>(p0);
+        const float4 b = *reinterpret_cast<const float4*>(p0 + slab);
+        const float4 c = *reinterpret_cast<const float4*>(p0 + 2 * slab);
+        const float4 e = *reinterpret_cast<const float4*>(p0 + 3 * slab);
+        v[0] = ((a.x + b.x) + c.x) + e.x;
+        v[1] = ((a.y + b.y) + c.y) + e.y;
+        v[2] = ((a.z + b.z) + c.z) + e.z;
+        v[3] = ((a.w + b.w) + c.w) + e.w;
+        if (logits) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) logits[t * 64 + 4 * sl + i] = v[i];
+        }
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) rows[tr][4 * sl + i] = v[i];
+    __syncthreads();
+    route_token_x16<KMAX>(&rows[tr][0], K, eps, mode, renorm, xt, t, valid, kout, ids, wout, h);
+    __syncthreads();
+    if (threadIdx.x < 64) hist[threadIdx.x * hist_ld + blockIdx.x] = h[threadIdx.x];
+}
+
 __global__ __launch_bounds__(256) void router_f32(const float* __restrict__ x,
                                                   const float* __restrict__ Wr, int64_t T,
                                                   int d, int N, float* __restrict__ logits) {
@@ -172,7 +337,7 @@ template <int NP, bool FULL, int KMAX>
 void launch_rr(const void* x, const void* Wr, int64_t T, int d, int N,
                const elb_route_params& p, float* logits, int* k, int* ids, float* w,
                hipStream_t s) {
-    hipLaunchKernelGGL((router_route_bf16<NP, FULL, KMAX>), dim3((unsigned)((T + 15) / 16)),
+    ELB_LAUNCH((router_route_bf16<NP, FULL, KMAX>), dim3((unsigned)((T + 15) / 16)),
                        dim3(64 * RW), 0, s, (const bf16_t*)x, (const bf16_t*)Wr, T, d, N, p.K,
                        p.eps, p.mode, p.renormalize, make_xtable(N), logits, k, ids, w);
 }
@@ -208,21 +373,49 @@ hipError_t launch_router_route(const void* x, const void* Wr, int64_t T, int d, 
     return hipGetLastError();
 }
 
+bool router_split_usable(int dtype, int64_t T, int d, int N, int K) {
+    return dtype == ELB_BF16 && N == 64 && K <= kLaneMaxK && T > kSmallBatch && d % 256 == 0 &&
+           d <= (1 << 20);
+}
+
+hipError_t launch_router_split_route(const void* x, const void* Wr, int64_t T, int d,
+                                     const elb_route_params& p, float* part, float* logits,
+                                     int* k, int* ids, float* w, int* hist, int64_t hist_ld,
+                                     hipStream_t s) {
+    if (T == 0) return hipSuccess;
+    const unsigned groups = (unsigned)((T + 63) / 64);
+    {
+        ProfileScope prof("router_split_bf16", s);
+        ELB_LAUNCH(router_split_bf16, dim3(groups, RW), dim3(256), 0, s,
+                           (const bf16_t*)x, (const bf16_t*)Wr, T, d, part);
+    }
+    ProfileScope prof("route_split_sum", s);
+    if (p.K <= 8)
+        ELB_LAUNCH(route_split_sum<8>, dim3(groups), dim3(1024), 0, s, part, T, p.K,
+                           p.eps, p.mode, p.renormalize, make_xtable(64), logits, k, ids, w,
+                           hist, hist_ld);
+    else
+        ELB_LAUNCH(route_split_sum<kLaneMaxK>, dim3(groups), dim3(1024), 0, s, part,
+                           T, p.K, p.eps, p.mode, p.renormalize, make_xtable(64), logits, k,
+                           ids, w, hist, hist_ld);
+    return hipGetLastError();
+}
+
 hipError_t launch_router(const void* x, const void* Wr, int64_t T, int d, int N, int dtype,
                          float* logits, hipStream_t s) {
     if (T == 0) return hipSuccess;
     if (dtype == ELB_BF16) {
         ProfileScope prof("router_bf16", s);
         if (T <= kSmallBatch)
-            hipLaunchKernelGGL(router_bf16<1>, dim3((unsigned)((T + 15) / 16), (unsigned)((N + 15) / 16)),
+            ELB_LAUNCH(router_bf16<1>, dim3((unsigned)((T + 15) / 16), (unsigned)((N + 15) / 16)),
                                dim3(64 * RW), 0, s, (const bf16_t*)x, (const bf16_t*)Wr, T, d,
                                N, logits);
         else
-            hipLaunchKernelGGL(router_bf16<4>, dim3((unsigned)((T + 15) / 16)), dim3(64 * RW), 0,
+            ELB_LAUNCH(router_bf16<4>, dim3((unsigned)((T + 15) / 16)), dim3(64 * RW), 0,
                                s, (const bf16_t*)x, (const bf16_t*)Wr, T, d, N, logits);
     } else {
         ProfileScope prof("router_f32", s);
-        hipLaunchKernelGGL(router_f32, dim3((unsigned)((T * N + 255) / 256)), dim3(256), 0, s,
+        ELB_LAUNCH(router_f32, dim3((unsigned)((T * N + 255) / 256)), dim3(256), 0, s,
                            (const float*)x, (const float*)Wr, T, d, N, logits);
     }
     return hipGetLastError();

@@ -10,7 +10,7 @@ from oracle import oracle as O
 from paper_2608_04401_amd import binding as B
 from paper_2608_04401_amd import synth
 
-from helpers import NEAR_TIE, cpu, to_gpu
+from helpers import NEAR_TIE, RTOL_BF16, cpu, rel_err_rows, to_gpu
 
 pytestmark = pytest.mark.gpu
 BF = torch.bfloat16
@@ -54,3 +54,30 @@ def test_fused_vs_oracle_olmoe():
     assert (ref.margin[~same] < NEAR_TIE).all()
     print("fused vs oracle: %d tokens, %d near-tie differences, mean k %.4f" % (
         len(k), int((~same).sum()), k.mean()))
+
+
+@pytest.mark.parametrize("T,d,K,mode", [(4096, 2048, 8, B.MODE_ELBOW), (1025, 512, 8, B.MODE_ELBOW),
+                                        (4097, 512, 8, B.MODE_TOPK), (2048, 256, 16, B.MODE_ELBOW),
+                                        (8256, 1024, 12, B.MODE_ELBOW), (3000, 768, 8, B.MODE_ELBOW)])
+def test_layer_split_router_equals_fused(T, d, K, mode):
+    """Large batches with N = 64 and d % 256 == 0: the layer computes the router in four blocks
+    per 64 tokens (each a quarter of the contraction) and routes in a second launch, which
+    also writes the dispatch histogram.  Its logits, k, ids and w must be the one-block fused
+    kernel's bits (slices of 1, 2, 3, 4 and 8 64-column chunks; ragged T; T = 8256 takes the
+    dispatch's scan launch), its per-expert counts those of its routing, and its outputs the
+    oracle's."""
+    L = synth.moe_layer(T, d, 64, 128, dtype="bf16", seed=T + d)
+    x, Wr, Wgu, Wd = (to_gpu(a, BF) for a in (L.x, L.W_router, L.W_gu, L.W_down))
+    y, dbg = B.elb_moe_forward(x, Wr, Wgu, Wd, K=K, mode=mode, debug=True)
+    k, ids, w, lg = B.elb_router_route(x, Wr, K=K, mode=mode, with_logits=True)
+    torch.cuda.synchronize()
+    assert torch.equal(dbg["logits"], lg)
+    assert torch.equal(dbg["k"], k) and torch.equal(dbg["ids"], ids) and torch.equal(dbg["w"], w)
+    kk, ii = cpu(k), cpu(ids)
+    assert np.array_equal(cpu(dbg["counts"]), np.bincount(ii[ii >= 0], minlength=64))
+    assert cpu(dbg["counts"]).sum() == kk.sum()
+    tok = np.sort(np.random.default_rng(T).choice(T, 256, replace=False))
+    ref = O.moe_experts(L.x, L.W_gu, L.W_down, kk[tok], ii[tok],
+                        cpu(w)[tok].astype(np.float64), tokens=tok)
+    rel = rel_err_rows(cpu(y)[tok], ref)
+    assert rel.max() < RTOL_BF16, rel.max()

@@ -30,7 +30,7 @@ def _check(x, Wr, Wgu, Wd, mode, label):
 
 def test_noalloc_matches_forward_on_consecutive_calls():
     """OLMoE-shaped layer (d = 2048, N = 64, intermediate 1024, bf16): T = 4096 (the largest
-    input run here; 201 MB of the 256 MiB scratch), then T = 64 (the decode-sized kernels,
+    input run here; 207 MB of the 256 MiB scratch), then T = 64 (the decode-sized kernels,
     reading a scratch that still holds the first call's data), then T = 4096 in top-8 mode."""
     Wr, Wgu, Wd = synth.device_stack_layer(0)
     x = synth.device_stack_input(4096, 2048)
