@@ -282,11 +282,13 @@ int elb_moe_forward_packed(const void *x, const void *W_router, const void *W_ga
 int64_t elb_calibrate_mfma_bf16(int32_t blocks, int32_t iters, float *out, void *stream);
 
 /*
- * Per-kernel timing (host-side hipEvents around each launch the library makes).
- * elb_profile_enable(1) starts recording on the calling process; every launch then
- * records a start/stop event pair on its stream (events without the system-scope fence, so
- * that recording them does not flush caches between kernels and slow the kernel that
- * follows).  elb_profile_read() synchronises on the
+ * Per-kernel timing (hipEvents attached to each launch the library makes).
+ * elb_profile_enable(1) starts recording on the calling process for every launch,
+ * elb_profile_enable(2) for the grouped expert GEMMs only, elb_profile_enable(0) stops; a
+ * recorded launch carries a start/stop event pair in its own dispatch
+ * (hipExtLaunchKernelGGL).  Timed launches run measurably slower than untimed back-to-back
+ * ones (on MI355X the large expert GEMMs by about 10 %), so per-kernel figures from this
+ * are upper bounds.  elb_profile_read() synchronises on the
  * recorded events, fills up to `cap` entries of names (static strings), total
  * milliseconds and launch counts per kernel, clears the records and returns the number
  * of kernels (or a negative elb_status).  Not for use under graph capture.

@@ -378,7 +378,8 @@ def elb_calibrate_mfma_bf16(blocks: int, iters: int) -> int:
     return int(n)
 
 
-def elb_profile_enable(on: bool = True) -> None:
+def elb_profile_enable(on=True) -> None:
+    """on: False/0 off, True/1 every launch, 2 the grouped expert GEMMs only."""
     _check("elb_profile_enable", lib().elb_profile_enable(int(on)))
 
 

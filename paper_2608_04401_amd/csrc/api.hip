@@ -4,6 +4,7 @@
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
+#include <cstring>
 #include <map>
 #include <mutex>
 #include <string>
@@ -167,7 +168,7 @@ struct Rec {
     int scope;  // the ProfileScope instance (a scope may make several launches)
     hipEvent_t a, b;
 };
-std::atomic<bool> g_prof_on{false};
+std::atomic<int> g_prof_on{0};  // 0 off, 1 every launch, 2 the grouped expert GEMMs only
 std::atomic<int> g_scope_seq{0};
 std::mutex g_prof_mu;
 std::vector<Rec> g_recs;
@@ -192,7 +193,8 @@ hipEvent_t pool_get() {
 
 ProfileScope::ProfileScope(const char* name, hipStream_t) : prev_name_(t_scope_name),
                                                             prev_id_(t_scope_id) {
-    if (g_prof_on.load(std::memory_order_relaxed)) {
+    const int lvl = g_prof_on.load(std::memory_order_relaxed);
+    if (lvl == 1 || (lvl == 2 && std::strncmp(name, "gemm_", 5) == 0)) {
         t_scope_name = name;
         t_scope_id = ++g_scope_seq;
     } else {
@@ -579,7 +581,8 @@ int64_t elb_calibrate_mfma_bf16(int32_t blocks, int32_t iters, float* out, void*
 }
 
 int elb_profile_enable(int on) {
-    g_prof_on.store(on != 0);
+    if (on < 0 || on > 2) return fail(ELB_ERR_INVALID_ARG, "profiling level %d outside [0, 2]", on);
+    g_prof_on.store(on);
     return ELB_OK;
 }
 

@@ -7,12 +7,12 @@
 //           multiple of 4).
 //   scan    one block per expert: an exclusive prefix over groups (the base of each group
 //           inside the expert's list) and the expert's total.
-//   scatter one lane per token again.  Each wave first forms the exclusive prefix of the
-//           expert totals (list offsets) and of their M-tile counts with a wave scan (block
-//           0 also writes them out); the rank of a token inside its group's share of expert
-//           e is the popcount of the expert's ballot below the lane, and its row is
-//           offsets[e] + base[e, group] + rank.  Rows within an expert are therefore in
-//           increasing token order.
+//   scatter one block of 4 waves per 64-token group, one lane per token.  Each wave forms
+//           the exclusive prefix of the expert totals (list offsets) and of their M-tile
+//           counts with a wave scan (block 0 also writes them out); the rank of a token inside
+//           its group's share of expert e is the popcount of the expert's ballot below the
+//           lane, and its row is offsets[e] + base[e, group] + rank (each wave takes a quarter
+//           of the experts).  Rows within an expert are therefore in increasing token order.
 // Up to kDirectGroups groups (T <= 8192) the scan launch is skipped: every scatter wave reads
 // its experts' whole histogram rows (lane e: row e, 16-byte loads all in flight at once) and
 // forms the expert totals and its own group's base itself.  One launch (dispatch_small) for
@@ -141,22 +141,26 @@ __global__ __launch_bounds__(1024) void dispatch_scan(int* __restrict__ hist, in
 }
 
 constexpr int kDirectGroups = 128;  // most groups whose histogram the scatter sums itself
+constexpr int kScatterWaves = 4;    // waves per 64-token group in the scatter
 
+// One block per 64-token group g; its kScatterWaves waves each place the group's tokens in the
+// lists of N / kScatterWaves experts, then each writes a share of the group's inv slots.
 // DIRECT: hist holds the raw per-group counts (no scan launch) and counts is written here
 template <bool DIRECT>
-__global__ __launch_bounds__(64 * kDispWaves) void dispatch_scatter(
+__global__ __launch_bounds__(64 * kScatterWaves) void dispatch_scatter(
     const int* __restrict__ k, const int* __restrict__ ids, int64_t T, int N, int K, int64_t ld,
     const int* __restrict__ hist, int* __restrict__ counts, int* __restrict__ offsets,
     int* __restrict__ tile_off, int* __restrict__ tail_list, TilePlan plan,
     int* __restrict__ row_token, int* __restrict__ inv) {
-    __shared__ int pos[kDispWaves][kWave][kWave + 1];
+    __shared__ int pos[kWave][kWave + 1];  // [token lane][expert]: the token's row
     const int lane = threadIdx.x & (kWave - 1);
     const int wv = threadIdx.x >> 6;
-    const int64_t g = (int64_t)blockIdx.x * kDispWaves + wv;
+    const int64_t g = blockIdx.x;
     const int64_t t = g * kWave + lane;
     const int64_t groups = (T + kWave - 1) / kWave;
-    // expert list offsets and M-tile offsets: exclusive prefixes over the experts (lane e).
-    // c: expert e's total; hist_mine: the base of this group inside expert e's list.
+    // expert list offsets and M-tile offsets: exclusive prefixes over the experts (lane e),
+    // formed by every wave.  c: expert e's total; hist_mine: the base of this group inside
+    // expert e's list.
     int c = 0, hist_mine = 0;
     if (DIRECT) {
         // lane e sums row e of the raw histogram: all of it (the total) and the groups below
@@ -184,7 +188,7 @@ __global__ __launch_bounds__(64 * kDispWaves) void dispatch_scatter(
         }
     } else {
         // the group's (scanned) histogram entry is loaded together with the totals (one
-        // memory round trip for both; surplus waves read group 0's, unused)
+        // memory round trip for both)
         c = (lane < N) ? counts[lane] : 0;
         hist_mine = (lane < N) ? hist[(int64_t)lane * ld + (g < groups ? g : 0)] : 0;
     }
@@ -213,35 +217,32 @@ __global__ __launch_bounds__(64 * kDispWaves) void dispatch_scatter(
         }
         write_tail_list(tail_mine, n_tail, lane, tail_list);
     }
-    if (g >= groups) return;  // wave-uniform; no block barrier in this kernel
+    if (g >= groups) return;  // block-uniform (T == 0: the one block only writes the offsets)
     const bool valid = t < T;
     const uint64_t mask = token_mask(k, ids, t, N, K, valid);
     // lane e holds the first row of expert e that belongs to this group
     const int base_mine = (lane < N) ? off_mine + hist_mine : 0;
     const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
-    for (int e = 0; e < N; ++e) {
+    const int per = (N + kScatterWaves - 1) / kScatterWaves;
+    const int e0 = wv * per, e1 = e0 + per < N ? e0 + per : N;
+    for (int e = e0; e < e1; ++e) {
         const bool has = (mask >> e) & 1ull;
         const uint64_t b = __ballot(has);
         const int base = __builtin_amdgcn_readlane(base_mine, e);  // e is wave-uniform
         if (has) {
             const int r = base + __popcll(b & below);
             row_token[r] = (int)t;
-            pos[wv][lane][e] = r;
+            pos[lane][e] = r;
         }
     }
-    if (!valid) return;
+    __syncthreads();
+    if (!valid) return;  // no barrier follows
     const int kt = k[t];
-    for (int j0 = 0; j0 < K; j0 += 8) {
-        int e8[8];
-        load_ids8(ids, t, K, j0, e8);
-#pragma unroll
-        for (int q = 0; q < 8; ++q) {
-            const int j = j0 + q, e = e8[q];
-            if (j >= K) break;
-            int r = -1;
-            if (j < kt && (unsigned)e < (unsigned)N) r = pos[wv][lane][e];
-            inv[t * K + j] = r;
-        }
+    for (int j = wv; j < K; j += kScatterWaves) {
+        const int e = ids[t * K + j];
+        int r = -1;
+        if (j < kt && (unsigned)e < (unsigned)N) r = pos[lane][e];
+        inv[t * K + j] = r;
     }
 }
 
@@ -366,14 +367,15 @@ hipError_t launch_dispatch(const int* k, const int* ids, int64_t T, int N, int K
     }
     {
         ProfileScope prof("dispatch_scatter", s);
+        const unsigned sblocks = (unsigned)(groups > 0 ? groups : 1);
         if (direct)
-            ELB_LAUNCH(dispatch_scatter<true>, dim3(blocks), dim3(64 * kDispWaves), 0,
-                               s, k, ids, T, N, K, ld, hist, counts, offsets, tile_off,
-                               tail_list, plan, row_token, inv);
+            ELB_LAUNCH(dispatch_scatter<true>, dim3(sblocks), dim3(64 * kScatterWaves), 0, s,
+                       k, ids, T, N, K, ld, hist, counts, offsets, tile_off, tail_list, plan,
+                       row_token, inv);
         else
-            ELB_LAUNCH(dispatch_scatter<false>, dim3(blocks), dim3(64 * kDispWaves), 0,
-                               s, k, ids, T, N, K, ld, hist, counts, offsets, tile_off,
-                               tail_list, plan, row_token, inv);
+            ELB_LAUNCH(dispatch_scatter<false>, dim3(sblocks), dim3(64 * kScatterWaves), 0, s,
+                       k, ids, T, N, K, ld, hist, counts, offsets, tile_off, tail_list, plan,
+                       row_token, inv);
     }
     return hipGetLastError();
 }
