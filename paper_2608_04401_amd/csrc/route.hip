@@ -50,26 +50,6 @@ __global__ __launch_bounds__(256) void route_kernel(const float* __restrict__ lo
 
 // ---- route_dma_kernel ----
 
-// LDS DMA layout of a wave's 64 x NP tile: P parts of CP 16-byte chunks per row; chunk cc of
-// part p of row r sits at 16-byte slot p 64 CP + r CP + (cc ^ swz(r)), so that for a fixed
-// chunk 16 consecutive rows fall in 16 distinct groups of 4 banks.
-constexpr int kRouteParts = 2;  // parts of the copy (a power of two)
-
-template <int NP>
-struct DmaTile {
-    static constexpr int C = NP / 4;              // 16-byte chunks per row
-    static constexpr int P = C >= kRouteParts ? kRouteParts : C;  // parts
-    static constexpr int CP = C / P;              // chunks per row per part
-    static constexpr int B = NP / P;              // floats per row per part
-    static constexpr int RPG = 16 / CP;           // rows per swizzle period
-    __device__ static int swz(int r) { return (r / RPG) % CP; }
-    // float index of value c (0 <= c < NP) of row r
-    __device__ static int at(int r, int c) {
-        const int p = c / B, cc = (c % B) / 4;
-        return ((p * 64 * CP + r * CP + (cc ^ swz(r))) << 2) + (c & 3);
-    }
-};
-
 template <int NP, int P, int G, int... I>
 __device__ __forceinline__ void sort_group(float* key, std::integer_sequence<int, I...>) {
     (compare_exchange<NP, PhasedHolder<NP, P>::net.idx[G][I]>(key), ...);

@@ -5,10 +5,11 @@
 //
 // The normalised curve runs from (0,0) to (1,1), as in the elbow-angle definition of
 // Section 2.3: p'_i = (p_(0) - p_(i)) / (p_(0) - p_(N-1) + eps), x'_i = i / (N - 1).
-// Arithmetic differs from the definition only by positive scaling and the sum's
+// Arithmetic differs from the definition only by positive scaling, a constant and the sum's
 // cancellation, which leave the argmax unchanged:
 //   u_i = exp(l_(i) - l_(0)) (so p_(i) = u_i / S, S = sum u), and
-//   D_i * (p_max - p_min + eps) * S = (1 - u_i) - x'_i * (1 - u_min + eps * S).
+//   D_i * (p_max - p_min + eps) * S = 1 - E_i,  E_i = u_i + x'_i * (1 - u_min + eps * S),
+// so the first argmax of D is the first argmin of E (one fma per point), with E_0 = 1.
 // The sort key is the fp32 logit itself (softmax is strictly increasing), with ties broken
 // by the lower expert id, so the ids and their order never depend on exp/division rounding.
 // The lane holds the token's N values in registers and sorts them with a compile-time
@@ -29,6 +30,14 @@ struct XTable {
 };
 
 constexpr float kLog2e = 1.4426950408889634f;
+
+// u = exp(l - l_max) = 2^(l log2(e) + nl) with the per-token constant nl = -(l_max log2(e)),
+// the exponent one fma: every kernel computes a token's u values this way, so all of them
+// give the same bits
+__device__ __forceinline__ float neg_scaled(float lmax) { return -(lmax * kLog2e); }
+__device__ __forceinline__ float rel_exp(float l, float nl) {
+    return __builtin_amdgcn_exp2f(fmaf(l, kLog2e, nl));
+}
 
 template <int NP>
 struct NetHolder {
@@ -122,6 +131,50 @@ __device__ __forceinline__ void stage_rows(const float* __restrict__ src, int N,
     }
 }
 
+// LDS DMA layout of a wave's 64 x NP tile: P parts of CP 16-byte chunks per row; chunk cc of
+// part p of row r sits at 16-byte slot p 64 CP + r CP + (cc ^ swz(r)), so that for a fixed
+// chunk 16 consecutive rows fall in 16 distinct groups of 4 banks.
+constexpr int kRouteParts = 2;  // parts of the copy (a power of two)
+
+template <int NP>
+struct DmaTile {
+    static constexpr int C = NP / 4;              // 16-byte chunks per row
+    static constexpr int P = C >= kRouteParts ? kRouteParts : C;  // parts
+    static constexpr int CP = C / P;              // chunks per row per part
+    static constexpr int B = NP / P;              // floats per row per part
+    static constexpr int RPG = 16 / CP;           // rows per swizzle period
+    __device__ static int swz(int r) { return (r / RPG) % CP; }
+    // float index of value c (0 <= c < NP) of row r
+    __device__ static int at(int r, int c) {
+        const int p = c / B, cc = (c % B) / 4;
+        return ((p * 64 * CP + r * CP + (cc ^ swz(r))) << 2) + (c & 3);
+    }
+};
+
+// Copy rows [0, rows) of a row-major 64 x NP fp32 tile at src (rows past `rows` repeat row
+// rows - 1, never used) into a wave's LDS tile in the DmaTile layout, with
+// global_load_lds_dwordx4 (whole 128-byte lines of every row per instruction; no registers);
+// part p of every row is issued before part p + 1.  The caller waits (vmcnt) before reading.
+template <int NP>
+__device__ __forceinline__ void dma_tile(const float* src, int rows, float* tile, int lane) {
+    using L = DmaTile<NP>;
+    const uint32_t lds0 = (uint32_t)(uintptr_t)(lds_void_t*)tile;
+#pragma unroll
+    for (int p = 0; p < L::P; ++p)
+#pragma unroll
+        for (int j = 0; j < L::CP; ++j) {
+            const int local = j * 64 + lane;
+            const int r = local / L::CP;
+            const int cc = (local % L::CP) ^ L::swz(r);
+            const int rs = r < rows ? r : rows - 1;
+            const uint32_t va = (uint32_t)(rs * NP + (p * L::CP + cc) * 4) * 4u;
+            const uint32_t la =
+                __builtin_amdgcn_readfirstlane(lds0 + (p * 64 * L::CP + j * 64) * 16);
+            asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2"
+                         :: "s"(la), "v"(va), "s"(src) : "memory", "m0");
+        }
+}
+
 // ---- the per-token steps, shared by every kernel that routes in one lane ----
 
 // u_i = exp(l_(i) - l_(0)) in rank order (0 for pads), S = sum u over the ranks (tree_sum),
@@ -131,9 +184,9 @@ __device__ __forceinline__ int sorted_elbow(const float (&key)[NP], int Nn, int 
                                             int mode, const XTable& xt, float (&u)[NP],
                                             float& S) {
     constexpr int KM = NP < KMAX ? NP : KMAX;
-    const float lmax = key[0];
+    const float nl = neg_scaled(key[0]);
 #pragma unroll
-    for (int i = 0; i < NP; ++i) u[i] = __builtin_amdgcn_exp2f((key[i] - lmax) * kLog2e);
+    for (int i = 0; i < NP; ++i) u[i] = rel_exp(key[i], nl);
     S = tree_sum<NP>(u);
     float umin = u[NP - 1];
     if (!FULL) {
@@ -142,27 +195,27 @@ __device__ __forceinline__ int sorted_elbow(const float (&key)[NP], int Nn, int 
     }
     int k = K;
     if (mode == ELB_MODE_ELBOW) {
-        // scaled deviation (1 - u_i) - x'_i (1 - u_min + eps S); D_0 == 0 exactly.  The first
-        // argmax only matters below K - 1 (beyond it k = K), so later points need only a max.
-        // Pads have x' = +inf and never win.
+        // E_i = u_i + x'_i (1 - u_min + eps S), E_0 = 1 (D_0 = 0).  The first argmin only
+        // matters below K - 1 (beyond it k = K), so later points need only a min.  Pads have
+        // x' = +inf and never win.
         const float Rp = (1.0f - umin) + eps * S;
-        float best = 0.f;
+        float best = 1.f;
         int e = 0;
-        float tail = -INFINITY;
+        float tail = INFINITY;
 #pragma unroll
         for (int i = 1; i < NP; ++i) {
-            const float Di = fmaf(-xt.x[i], Rp, 1.0f - u[i]);
+            const float Ei = fmaf(xt.x[i], Rp, u[i]);
             if (i < KM - 1) {
                 const bool head = i < K - 1;
-                const bool better = head && (Di > best);  // strict: first index wins ties
-                best = better ? Di : best;
+                const bool better = head && (Ei < best);  // strict: first index wins ties
+                best = better ? Ei : best;
                 e = better ? i : e;
-                tail = head ? tail : fmaxf(tail, Di);
+                tail = head ? tail : fminf(tail, Ei);
             } else {
-                tail = fmaxf(tail, Di);
+                tail = fminf(tail, Ei);
             }
         }
-        k = (tail > best) ? K : e + 1;
+        k = (tail < best) ? K : e + 1;
     }
     return k;
 }
@@ -233,7 +286,7 @@ __device__ __forceinline__ void select_emit(const float (&key)[NP], OKey&& okey,
                                             const float (&u)[NP], float S, int renorm,
                                             Emit&& emit) {
     constexpr int KM = NP < KMAX ? NP : KMAX;
-    const float lmax = key[0];
+    const float nl = neg_scaled(key[0]);
     const uint64_t sel = select_first_k<NP, KM>(key, okey, Nn, k);
     int cid[KM];
     float ck[KM];
@@ -256,7 +309,7 @@ __device__ __forceinline__ void select_emit(const float (&key)[NP], OKey&& okey,
                 if (q < r) rank += (q < k && ck[q] >= ck[r]) ? 1 : 0;
                 if (q > r) rank += (q < k && ck[q] > ck[r]) ? 1 : 0;
             }
-            emit(rank, cid[r], __builtin_amdgcn_exp2f((ck[r] - lmax) * kLog2e) * inv);
+            emit(rank, cid[r], rel_exp(ck[r], nl) * inv);
         }
     }
 #pragma unroll
@@ -369,10 +422,10 @@ __device__ __forceinline__ void route_token_x16(float* row, int K, float eps, in
         key[i] = __int_as_float(ord_flip32((int)(v[i] >> 32)));
         id[i] = NP - 1 - (int)(uint32_t)v[i];
     }
-    const float lmax = __shfl(key[0], 0, 16);
+    const float nl = neg_scaled(__shfl(key[0], 0, 16));
     float u[4];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) u[i] = __builtin_amdgcn_exp2f((key[i] - lmax) * kLog2e);
+    for (int i = 0; i < 4; ++i) u[i] = rel_exp(key[i], nl);
     // ---- S over the ranks (tree_sum by a butterfly), u_min = u of rank 63 ----
     float S = (u[0] + u[1]) + (u[2] + u[3]);
 #pragma unroll
@@ -381,21 +434,21 @@ __device__ __forceinline__ void route_token_x16(float* row, int K, float eps, in
     int k = K;
     if (mode == ELB_MODE_ELBOW) {
         const float Rp = (1.0f - umin) + eps * S;
-        float bd = (sl == 0) ? 0.f : -INFINITY;  // D_0 == 0 exactly
+        float bd = (sl == 0) ? 1.f : INFINITY;  // E_0 = 1
         int be = (sl == 0) ? 0 : NP;
-        float tail = -INFINITY;
+        float tail = INFINITY;
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
             const int r = 4 * sl + i;
             if (r == 0) continue;
-            const float Di = fmaf(-xt.x[r], Rp, 1.0f - u[i]);
+            const float Ei = fmaf(xt.x[r], Rp, u[i]);
             if (r < K - 1) {
-                if (Di > bd) {  // strict: ranks rise with i, so the first index wins ties
-                    bd = Di;
+                if (Ei < bd) {  // strict: ranks rise with i, so the first index wins ties
+                    bd = Ei;
                     be = r;
                 }
             } else {
-                tail = fmaxf(tail, Di);
+                tail = fminf(tail, Ei);
             }
         }
 #pragma unroll
@@ -403,13 +456,13 @@ __device__ __forceinline__ void route_token_x16(float* row, int K, float eps, in
             const float obd = __shfl_xor(bd, m, 16);
             const int obe = __shfl_xor(be, m, 16);
             const float ot = __shfl_xor(tail, m, 16);
-            if (obd > bd || (obd == bd && obe < be)) {
+            if (obd < bd || (obd == bd && obe < be)) {
                 bd = obd;
                 be = obe;
             }
-            tail = fmaxf(tail, ot);
+            tail = fminf(tail, ot);
         }
-        k = (tail > bd) ? K : be + 1;
+        k = (tail < bd) ? K : be + 1;
     }
     float denom = S;
     if (renorm) {  // the selected ranks' u, the others as exact zeros, in the same tree

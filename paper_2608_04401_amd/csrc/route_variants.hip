@@ -6,8 +6,8 @@
 // One LANE per token with the routing kernel's staging and arithmetic (route_lane.h), but the
 // sorting network carries the expert ids along with the logits, so the id at every rank is
 // known and any cap up to N costs the same.  Same bits as the routing kernel: the same keys,
-// u_i = exp(l_(i) - l_(0)) in rank order, S as the same tree over the ranks (tree_sum), the
-// same scaled deviation and first argmax, w = u * (1 / denominator).  The elbow angle (no selection asked for) and
+// u_i = exp(l_(i) - l_(0)) in rank order (rel_exp), S as the same tree over the ranks
+// (tree_sum), the same E_i and first argmin, w = u * (1 / denominator).  The elbow angle (no selection asked for) and
 // tail randomisation with K <= 16 sort the keys only.
 #include "route_lane.h"
 
@@ -110,10 +110,10 @@ __global__ __launch_bounds__(256) void route_pair_kernel(
     }
 
     // ---- u, S, u_min and the elbow: the routing kernel's arithmetic, in rank order ----
-    const float lmax = key[0];
+    const float nl = neg_scaled(key[0]);
     float u[NP];
 #pragma unroll
-    for (int i = 0; i < NP; ++i) u[i] = __builtin_amdgcn_exp2f((key[i] - lmax) * kLog2e);
+    for (int i = 0; i < NP; ++i) u[i] = rel_exp(key[i], nl);
     const float S = tree_sum<NP>(u);
     float umin = u[NP - 1];
     if (!FULL) {
@@ -121,13 +121,13 @@ __global__ __launch_bounds__(256) void route_pair_kernel(
         for (int i = 0; i < NP; ++i) umin = (i == Nn - 1) ? u[i] : umin;
     }
     const float Rp = (1.0f - umin) + eps * S;
-    float best = 0.f;  // D_0 == 0 exactly
+    float best = 1.f;  // E_0 = 1 (D_0 = 0)
     int e = 0;
 #pragma unroll
     for (int i = 1; i < NP; ++i) {
-        const float Di = fmaf(-xt.x[i], Rp, 1.0f - u[i]);  // pads: x' = +inf, never win
-        const bool better = Di > best;  // strict: the first index wins ties
-        best = better ? Di : best;
+        const float Ei = fmaf(xt.x[i], Rp, u[i]);  // pads: x' = +inf, never win
+        const bool better = Ei < best;  // strict: the first index wins ties
+        best = better ? Ei : best;
         e = better ? i : e;
     }
     if (eout && active) eout[t] = e;
@@ -186,7 +186,7 @@ __global__ __launch_bounds__(256) void route_pair_kernel(
                 bc = ok ? c : bc;
             }
             taken |= 1ull << bc;
-            const float ub = __builtin_amdgcn_exp2f((order_key(row[bc]) - lmax) * kLog2e);
+            const float ub = rel_exp(order_key(row[bc]), nl);
             if (active) {
                 ids[t * K + j] = bc;
                 wout[t * K + j] = ub;
@@ -206,7 +206,7 @@ __global__ __launch_bounds__(256) void route_pair_kernel(
                     if (q > r) rank += (q < k && ck[q] > ck[r]) ? 1 : 0;
                 }
                 ids[t * K + rank] = cid[r];
-                wout[t * K + rank] = __builtin_amdgcn_exp2f((ck[r] - lmax) * kLog2e) * inv;
+                wout[t * K + rank] = rel_exp(ck[r], nl) * inv;
             }
         }
         for (int j = k; j < K; ++j) wout[t * K + j] *= inv;  // this lane's own writes
@@ -243,7 +243,7 @@ __global__ __launch_bounds__(256) void route_pair_kernel(
                 bc = ok ? c : bc;
             }
             taken |= 1ull << bc;
-            const float ub = __builtin_amdgcn_exp2f((order_key(row[bc]) - lmax) * kLog2e);
+            const float ub = rel_exp(order_key(row[bc]), nl);
             if (active) {
                 ids[t * K + j] = bc;
                 wout[t * K + j] = ub;

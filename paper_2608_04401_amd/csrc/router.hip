@@ -177,9 +177,9 @@ __global__ __launch_bounds__(64 * RW) void router_route_bf16(
 // 64 KB of x and 64 KB of W_r at d = 2048, instead of the 256 KB of W_r that every 16-token
 // block of the one-block kernel streams.  Wave w multiplies tokens [16 w, 16 w + 16) by all
 // 64 experts.  The partials go to part[s][t][n] (workspace).
-// route_split_sum: block of 64 tokens (16 waves, 16 lanes per token): the four partials
-// summed in order (the logit), then route_token_x16; the block also writes its group's
-// per-expert assignment count (the dispatch histogram column of these 64 tokens).
+// route_split_sum: one wave per 64 tokens, one lane per token: the four partials summed in
+// order (the logit), then the routing kernel's per-lane code; the wave also writes its
+// group's per-expert assignment counts (the dispatch histogram column of these 64 tokens).
 // Requires N == 64 and d % 256 == 0 (every slice a whole number of 64-column chunks).
 constexpr int kSplitRing = 8;                // chunks in the ring (128 KB of LDS)
 constexpr int kSplitSlot = 2 * 64 * 128;     // bytes per chunk: 64 W_r rows, then 64 x rows
@@ -276,47 +276,78 @@ __global__ __launch_bounds__(256) void router_split_bf16(const bf16_t* __restric
         }
 }
 
+// route_split_sum: one wave per 64-token group, one lane per token.  The group's four partial
+// tiles (64 x 64 fp32 each) are copied into LDS with global_load_lds (the routing kernel's
+// swizzled tile layout), each lane sums its token's four rows in order -- the logits -- and
+// routes them with the routing kernel's own per-lane code (the same bits), then the group's
+// per-expert assignment counts are written to its histogram column.
 template <int KMAX>
-__global__ __launch_bounds__(1024) void route_split_sum(const float* __restrict__ part,
-                                                        int64_t T, int K, float eps, int mode,
-                                                        int renorm, XTable xt,
-                                                        float* __restrict__ logits,
-                                                        int* __restrict__ kout,
-                                                        int* __restrict__ ids,
-                                                        float* __restrict__ wout,
-                                                        int* __restrict__ hist,
-                                                        int64_t hist_ld) {
-    __shared__ float rows[64][65];
+__global__ __launch_bounds__(64) void route_split_sum(const float* __restrict__ part,
+                                                      int64_t T, int K, float eps, int mode,
+                                                      int renorm, XTable xt,
+                                                      float* __restrict__ logits,
+                                                      int* __restrict__ kout,
+                                                      int* __restrict__ ids,
+                                                      float* __restrict__ wout,
+                                                      int* __restrict__ hist,
+                                                      int64_t hist_ld) {
+    using L = DmaTile<64>;
+    constexpr int NP = 64, TILE = 64 * 64;
+    __shared__ __attribute__((aligned(1024))) float lds[4 * TILE];
     __shared__ int h[64];
+    const int lane = threadIdx.x;
     const int64_t t0 = (int64_t)blockIdx.x * 64;
-    const int tr = threadIdx.x >> 4, sl = threadIdx.x & 15;
-    if (threadIdx.x < 64) h[threadIdx.x] = 0;
-    const int64_t t = t0 + tr;
-    const bool valid = t < T;
-    // experts 4 sl .. 4 sl + 3 of token t: ((P_0 + P_1) + P_2) + P_3
-    float v[4] = {0.f, 0.f, 0.f, 0.f};  // rows past T: finite, never stored
-    if (valid) {
-        const int64_t slab = T * 64;
-        const float* p0 = part + t * 64 + 4 * sl;
-        const float4 a = *reinterpret_cast<const float4*>(p0);
-        const float4 b = *reinterpret_cast<const float4*>(p0 + slab);
-        const float4 c = *reinterpret_cast<const float4*>(p0 + 2 * slab);
-        const float4 e = *reinterpret_cast<const float4*>(p0 + 3 * slab);
-        v[0] = ((a.x + b.x) + c.x) + e.x;
-        v[1] = ((a.y + b.y) + c.y) + e.y;
-        v[2] = ((a.z + b.z) + c.z) + e.z;
-        v[3] = ((a.w + b.w) + c.w) + e.w;
-        if (logits) {
+    const int rows = (int)((T - t0) < 64 ? (T - t0) : 64);
+    h[lane] = 0;
 #pragma unroll
-            for (int i = 0; i < 4; ++i) logits[t * 64 + 4 * sl + i] = v[i];
-        }
+    for (int q = 0; q < 4; ++q) dma_tile<NP>(part + ((int64_t)q * T + t0) * NP, rows,
+                                             lds + q * TILE, lane);
+    ELB_WAIT_VMCNT(0);
+    __builtin_amdgcn_s_barrier();  // one wave: orders the copies' LDS writes before the reads
+    // the token's logits: ((P0 + P1) + P2) + P3, element by element
+    auto logit = [&](int c) {
+        const int a = L::at(lane, c);
+        return ((lds[a] + lds[TILE + a]) + lds[2 * TILE + a]) + lds[3 * TILE + a];
+    };
+    float key[NP], okey[NP];
+#pragma unroll
+    for (int c = 0; c < NP; ++c) okey[c] = logit(c);
+    const bool valid = lane < rows;
+    const int64_t t = t0 + lane;
+    if (logits && valid) {  // the sums as they are (the one-block kernels write the same)
+#pragma unroll
+        for (int c = 0; c < NP; ++c) logits[t * NP + c] = okey[c];
     }
 #pragma unroll
-    for (int i = 0; i < 4; ++i) rows[tr][4 * sl + i] = v[i];
-    __syncthreads();
-    route_token_x16<KMAX>(&rows[tr][0], K, eps, mode, renorm, xt, t, valid, kout, ids, wout, h);
-    __syncthreads();
-    if (threadIdx.x < 64) hist[threadIdx.x * hist_ld + blockIdx.x] = h[threadIdx.x];
+    for (int c = 0; c < NP; ++c) {
+        okey[c] = order_key(okey[c]);
+        key[c] = okey[c];
+    }
+    sort_desc<NP>(key, std::make_integer_sequence<int, NetHolder<NP>::net.n>{});
+    float u[NP], S;
+    const int k = sorted_elbow<NP, true, KMAX>(key, NP, K, eps, mode, xt, u, S);
+    if (valid) kout[t] = k;
+    // outputs staged in the lane's own row of tile 0 (every read of the tiles precedes, in
+    // program order, every write below; a wave's LDS operations complete in order)
+    int* const stg_i = reinterpret_cast<int*>(lds);
+    float* const stg_w = lds + 64 * (KMAX + 1);
+    const int ld = K + 1;
+    select_emit<NP, true, KMAX>(
+        key, [&](int c) { return okey[c]; }, [&](int c) { return order_key(logit(c)); }, NP, K,
+        k, u, S, renorm, [&](int j, int id, float w) {
+            stg_i[lane * ld + j] = id;
+            stg_w[lane * ld + j] = w;
+            if (valid && id >= 0) atomicAdd(&h[id], 1);
+        });
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    hist[lane * hist_ld + blockIdx.x] = h[lane];
+    if (!valid) return;
+    for (int j = 0; j < K; ++j) {
+        ids[t * K + j] = stg_i[lane * ld + j];
+        wout[t * K + j] = stg_w[lane * ld + j];
+    }
 }
 
 __global__ __launch_bounds__(256) void router_f32(const float* __restrict__ x,
@@ -391,13 +422,12 @@ hipError_t launch_router_split_route(const void* x, const void* Wr, int64_t T, i
     }
     ProfileScope prof("route_split_sum", s);
     if (p.K <= 8)
-        ELB_LAUNCH(route_split_sum<8>, dim3(groups), dim3(1024), 0, s, part, T, p.K,
-                           p.eps, p.mode, p.renormalize, make_xtable(64), logits, k, ids, w,
-                           hist, hist_ld);
+        ELB_LAUNCH(route_split_sum<8>, dim3(groups), dim3(64), 0, s, part, T, p.K, p.eps,
+                   p.mode, p.renormalize, make_xtable(64), logits, k, ids, w, hist, hist_ld);
     else
-        ELB_LAUNCH(route_split_sum<kLaneMaxK>, dim3(groups), dim3(1024), 0, s, part,
-                           T, p.K, p.eps, p.mode, p.renormalize, make_xtable(64), logits, k,
-                           ids, w, hist, hist_ld);
+        ELB_LAUNCH(route_split_sum<kLaneMaxK>, dim3(groups), dim3(64), 0, s, part, T, p.K,
+                   p.eps, p.mode, p.renormalize, make_xtable(64), logits, k, ids, w, hist,
+                   hist_ld);
     return hipGetLastError();
 }
 
