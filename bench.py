@@ -185,8 +185,14 @@ def routing_only(B, torch, T=65536, N=64, K=8, nbuf=32, iters=64, big_T=0):
         call = lambda b: L.elb_route(C.c_void_p(b.data_ptr()), big_T, N, C.byref(p),
                                      C.c_void_p(k2.data_ptr()), C.c_void_p(ids2.data_ptr()),
                                      C.c_void_p(w2.data_ptr()), st)
-        for i in range(4):
+        # about 0.3 s of untimed calls first: the first launches on a fresh pair of buffers
+        # run up to ~10 % slow (clocks and caches settling)
+        i, t_w = 0, time.perf_counter()
+        while time.perf_counter() - t_w < 0.3:
             call(bufs2[i % 2])
+            i += 1
+            if i % 8 == 0:
+                torch.cuda.synchronize()
         torch.cuda.synchronize()
         B.elb_profile_read()
         B.elb_profile_enable(True)
@@ -200,14 +206,19 @@ def routing_only(B, torch, T=65536, N=64, K=8, nbuf=32, iters=64, big_T=0):
         out["T_2^20"] = {"us": round(us2, 2), "bytes": nb2,
                          "GB/s": round(nb2 / (us2 * 1e-6) / 1e9, 1),
                          "frac": round(nb2 / (us2 * 1e-6) / 1e9 / PEAK_HBM_GBS, 4)}
-        e0.record()
-        for i in range(16):
-            call(bufs2[i % 2])
-        e1.record()
-        torch.cuda.synchronize()
-        us2b = e0.elapsed_time(e1) / 16 * 1e3
+        blk = []
+        for _ in range(3):
+            torch.cuda.synchronize()
+            e0.record()
+            for i in range(16):
+                call(bufs2[i % 2])
+            e1.record()
+            torch.cuda.synchronize()
+            blk.append(e0.elapsed_time(e1) / 16 * 1e3)
+        us2b = float(np.median(blk))
         out["T_2^20"]["back_to_back"] = {
-            "us": round(us2b, 2), "GB/s": round(nb2 / (us2b * 1e-6) / 1e9, 1),
+            "us": round(us2b, 2), "blocks_us": [round(v, 2) for v in blk],
+            "GB/s": round(nb2 / (us2b * 1e-6) / 1e9, 1),
             "frac": round(nb2 / (us2b * 1e-6) / 1e9 / PEAK_HBM_GBS, 4)}
         del lg2, bufs2, k2, ids2, w2
     # variable-k dispatch of that routing (histogram, scan, scatter)
