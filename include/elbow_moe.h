@@ -223,7 +223,7 @@ int elb_moe_forward(const void *x, const void *W_router, const void *W_gate_up,
  * Limits and behaviour:
  *  - a problem whose elb_moe_workspace_bytes(T, d, N, m, K, dtype) exceeds
  *    ELB_NOALLOC_SCRATCH_BYTES is rejected with ELB_ERR_UNSUPPORTED before anything is
- *    enqueued (the OLMoE-shaped layer, d = 2048, N = 64, m = 1024, K = 8, fits up to 5308
+ *    enqueued (the OLMoE-shaped layer, d = 2048, N = 64, m = 1024, K = 8, fits up to 5307
  *    tokens);
  *  - nothing in the scratch has to start at zero, and nothing is cleared;
  *  - every call on one GPU uses that GPU's one array, so calls that overlap in time on one

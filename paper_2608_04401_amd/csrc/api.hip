@@ -54,7 +54,8 @@ Layout layout(int64_t T, int d, int N, int m, int K, int dtype) {
         return at;
     };
     const size_t rows = (size_t)T * K;
-    L.hist = take((size_t)dispatch_hist_ints(T, N) * 4);
+    // the split router's routing may write split_hist_subs(T) histograms
+    L.hist = take((size_t)dispatch_hist_ints(T, N) * split_hist_subs(T) * 4);
     L.tile_off = take((size_t)(N + 1 + kTailMax + 1) * 4);  // tile_off, then tail_list
     L.counts = take((size_t)N * 4);
     L.offsets = take((size_t)(N + 1) * 4);
@@ -363,7 +364,7 @@ static int experts_impl(const void* x, const void* W_gate_up, const void* W_down
                         const int32_t* k, const int32_t* ids, const float* w,
                         const void* residual, int64_t T, int d, int N, int m, int K, int dtype,
                         void* y, char* ws, const Layout& L, int32_t* counts_out,
-                        hipStream_t s, bool hist_ready = false) {
+                        hipStream_t s, bool hist_ready = false, int hist_subs = 1) {
     int* hist = (int*)(ws + L.hist);
     int* tile_off = (int*)(ws + L.tile_off);
     int* counts = counts_out ? counts_out : (int*)(ws + L.counts);
@@ -391,7 +392,8 @@ static int experts_impl(const void* x, const void* W_gate_up, const void* W_down
                           "combine");
     }
     if (int rc = hip_status(launch_dispatch(k, ids, T, N, K, counts, offsets, row_token, inv,
-                                            hist, tile_off, tail_list, plan, s, hist_ready),
+                                            hist, tile_off, tail_list, plan, s, hist_ready,
+                                            hist_subs),
                             "dispatch"))
         return rc;
     {
@@ -485,7 +487,7 @@ static int moe_forward_entry(const void* x, const void* W_router, const void* W_
                 "router_split_route"))
             return rc;
         return experts_impl(x, W_gate_up, W_down, packed, k, ids, w, residual, T, d, N, m, K,
-                            dtype, y, ws, L, counts_out, s, true);
+                            dtype, y, ws, L, counts_out, s, true, split_hist_subs(T));
     }
     if (router_route_fusable(dtype, K) && !(N == 64 && T <= kSmallBatch)) {
         if (int rc = hip_status(launch_router_route(x, W_router, T, d, N, *params, logits_out,

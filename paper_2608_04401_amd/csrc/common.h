@@ -56,6 +56,15 @@ hipError_t launch_route_pair(const float* logits, const float* rand, int64_t T, 
 inline int64_t dispatch_groups(int64_t T) { return (T + kWave - 1) / kWave; }
 inline int64_t dispatch_hist_ld(int64_t T) { return (dispatch_groups(T) + 3) & ~(int64_t)3; }
 inline int64_t dispatch_hist_ints(int64_t T, int N) { return dispatch_hist_ld(T) * N; }
+// up to this many groups the scatter sums the histogram itself (no scan launch)
+constexpr int64_t kDirectGroups = 128;
+// the split router's routing for T <= 64 kDirectGroups runs 16 tokens per block and writes
+// one histogram per quarter of each 64-token group: kHistSubs histograms [N, hist_ld], one
+// after the other, which the scatter adds up
+constexpr int kHistSubs = 4;
+inline int split_hist_subs(int64_t T) {
+    return dispatch_groups(T) <= kDirectGroups ? kHistSubs : 1;
+}
 
 // M-tiling of the grouped GEMMs, computed by the dispatch on the device from the counts.
 // Each expert gets ceil(c / tile_rows) M-tiles, except that with tail_rows > 0 an expert with
@@ -74,11 +83,12 @@ constexpr int kTailRows = 32;  // largest remainder the tail kernel takes
 // hist: dispatch_hist_ints(T, N) int32 scratch ([N, dispatch_hist_ld(T)], expert-major);
 // tile_off [N + 1]; tail_list [kTailMax + 1]
 // hist_ready: hist already holds the per-group counts (written by the split router), so the
-// count launch is skipped
+// count launch is skipped; hist_subs: how many histograms it holds (split_hist_subs(T) from
+// the split router, else 1)
 hipError_t launch_dispatch(const int* k, const int* ids, int64_t T, int N, int K, int* counts,
                            int* offsets, int* row_token, int* inv, int* hist, int* tile_off,
                            int* tail_list, const TilePlan& plan, hipStream_t s,
-                           bool hist_ready = false);
+                           bool hist_ready = false, int hist_subs = 1);
 
 // router logits
 hipError_t launch_router(const void* x, const void* Wr, int64_t T, int d, int N, int dtype,
@@ -93,8 +103,8 @@ hipError_t launch_router_route(const void* x, const void* Wr, int64_t T, int d, 
 // the layer's router and routing for large batches in two launches (N == 64, bf16, K <=
 // kLaneMaxK, T > kSmallBatch, d % 256 == 0): partial logits per quarter of the contraction
 // into part [4, T, 64] (workspace), then their sum and the routing; also writes the dispatch
-// histogram (hist [64, hist_ld], column g = tokens [64 g, 64 g + 64)).  Same bits as the other
-// router paths.
+// histogram: split_hist_subs(T) histograms [64, hist_ld] (column g = tokens [64 g, 64 g + 64),
+// or its quarter j in histogram j).  Same bits as the other router paths.
 bool router_split_usable(int dtype, int64_t T, int d, int N, int K);
 hipError_t launch_router_split_route(const void* x, const void* Wr, int64_t T, int d,
                                      const elb_route_params& p, float* part, float* logits,

@@ -15,8 +15,10 @@
 //           of the experts).  Rows within an expert are therefore in increasing token order.
 // Up to kDirectGroups groups (T <= 8192) the scan launch is skipped: every scatter wave reads
 // its experts' whole histogram rows (lane e: row e, 16-byte loads all in flight at once) and
-// forms the expert totals and its own group's base itself.  One launch (dispatch_small) for
-// T <= 256.  All three forms give the same rows.
+// forms the expert totals and its own group's base itself.  When the split router's routing
+// wrote one histogram per quarter of each group (kHistSubs of them), wave w reads histogram w
+// and the four waves add their sums through LDS.  One launch (dispatch_small) for T <= 256.
+// All three forms give the same rows.
 // Requires N <= 64 (one mask bit per expert).
 #include "common.h"
 
@@ -140,19 +142,22 @@ __global__ __launch_bounds__(1024) void dispatch_scan(int* __restrict__ hist, in
     if (tid == 0) counts[e] = total;
 }
 
-constexpr int kDirectGroups = 128;  // most groups whose histogram the scatter sums itself
-constexpr int kScatterWaves = 4;    // waves per 64-token group in the scatter
+constexpr int kScatterWaves = 4;  // waves per 64-token group in the scatter
+static_assert(kScatterWaves == kHistSubs, "one scatter wave per sub-histogram");
 
 // One block per 64-token group g; its kScatterWaves waves each place the group's tokens in the
 // lists of N / kScatterWaves experts, then each writes a share of the group's inv slots.
-// DIRECT: hist holds the raw per-group counts (no scan launch) and counts is written here
+// DIRECT: hist holds the raw per-group counts (no scan launch) and counts is written here;
+// subs (DIRECT only): the number of histograms (kHistSubs: one per quarter of each group,
+// sub_stride ints apart, summed here; 1: every wave reads the one histogram)
 template <bool DIRECT>
 __global__ __launch_bounds__(64 * kScatterWaves) void dispatch_scatter(
     const int* __restrict__ k, const int* __restrict__ ids, int64_t T, int N, int K, int64_t ld,
-    const int* __restrict__ hist, int* __restrict__ counts, int* __restrict__ offsets,
-    int* __restrict__ tile_off, int* __restrict__ tail_list, TilePlan plan,
-    int* __restrict__ row_token, int* __restrict__ inv) {
+    const int* __restrict__ hist, int subs, int64_t sub_stride, int* __restrict__ counts,
+    int* __restrict__ offsets, int* __restrict__ tile_off, int* __restrict__ tail_list,
+    TilePlan plan, int* __restrict__ row_token, int* __restrict__ inv) {
     __shared__ int pos[kWave][kWave + 1];  // [token lane][expert]: the token's row
+    __shared__ int red[2][kScatterWaves][kWave];  // per-wave sums of the sub-histograms
     const int lane = threadIdx.x & (kWave - 1);
     const int wv = threadIdx.x >> 6;
     const int64_t g = blockIdx.x;
@@ -165,8 +170,10 @@ __global__ __launch_bounds__(64 * kScatterWaves) void dispatch_scatter(
     if (DIRECT) {
         // lane e sums row e of the raw histogram: all of it (the total) and the groups below
         // g (the base), in group order; pads past `groups` are not read as counts
+        const int sub = subs > 1 ? wv : 0;  // wave wv reads histogram wv (or the only one)
         if (lane < N) {
-            const int4* h4 = reinterpret_cast<const int4*>(hist + (int64_t)lane * ld);
+            const int4* h4 =
+                reinterpret_cast<const int4*>(hist + sub * sub_stride + (int64_t)lane * ld);
             const int n4 = (int)(ld >> 2), ng = (int)groups, gg = (int)g;
             int4 v[kDirectGroups / 4];
 #pragma unroll
@@ -184,6 +191,18 @@ __global__ __launch_bounds__(64 * kScatterWaves) void dispatch_scatter(
                     c += x;
                     hist_mine += gi < gg ? x : 0;
                 }
+            }
+        }
+        if (subs > 1) {  // block-uniform: every wave takes the sums over the histograms
+            red[0][wv][lane] = c;
+            red[1][wv][lane] = hist_mine;
+            __syncthreads();
+            c = 0;
+            hist_mine = 0;
+#pragma unroll
+            for (int q = 0; q < kScatterWaves; ++q) {
+                c += red[0][q][lane];
+                hist_mine += red[1][q][lane];
             }
         }
     } else {
@@ -342,7 +361,7 @@ __global__ __launch_bounds__(256) void dispatch_small(const int* __restrict__ k,
 hipError_t launch_dispatch(const int* k, const int* ids, int64_t T, int N, int K, int* counts,
                            int* offsets, int* row_token, int* inv, int* hist, int* tile_off,
                            int* tail_list, const TilePlan& plan, hipStream_t s,
-                           bool hist_ready) {
+                           bool hist_ready, int hist_subs) {
     if (T <= 256 && !hist_ready) {
         ProfileScope prof("dispatch_small", s);
         ELB_LAUNCH(dispatch_small, dim3(1), dim3(256), 0, s, k, ids, (int)T, N, K,
@@ -352,6 +371,8 @@ hipError_t launch_dispatch(const int* k, const int* ids, int64_t T, int N, int K
     const int64_t groups = dispatch_groups(T);
     const int64_t ld = dispatch_hist_ld(T);
     const bool direct = groups <= kDirectGroups;
+    if (hist_subs != 1 && !(hist_ready && direct && hist_subs == kHistSubs))
+        return hipErrorInvalidValue;  // sub-histograms come from the split router, T <= 8192
     // at least one scatter block, which also writes offsets and tile_off (also when T == 0)
     const int64_t nb = (groups + kDispWaves - 1) / kDispWaves;
     const unsigned blocks = (unsigned)(nb > 0 ? nb : 1);
@@ -370,12 +391,12 @@ hipError_t launch_dispatch(const int* k, const int* ids, int64_t T, int N, int K
         const unsigned sblocks = (unsigned)(groups > 0 ? groups : 1);
         if (direct)
             ELB_LAUNCH(dispatch_scatter<true>, dim3(sblocks), dim3(64 * kScatterWaves), 0, s,
-                       k, ids, T, N, K, ld, hist, counts, offsets, tile_off, tail_list, plan,
-                       row_token, inv);
+                       k, ids, T, N, K, ld, hist, hist_subs, ld * N, counts, offsets,
+                       tile_off, tail_list, plan, row_token, inv);
         else
             ELB_LAUNCH(dispatch_scatter<false>, dim3(sblocks), dim3(64 * kScatterWaves), 0, s,
-                       k, ids, T, N, K, ld, hist, counts, offsets, tile_off, tail_list, plan,
-                       row_token, inv);
+                       k, ids, T, N, K, ld, hist, 1, ld * N, counts, offsets, tile_off,
+                       tail_list, plan, row_token, inv);
     }
     return hipGetLastError();
 }

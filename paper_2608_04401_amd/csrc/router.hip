@@ -350,6 +350,58 @@ __global__ __launch_bounds__(64) void route_split_sum(const float* __restrict__ 
     }
 }
 
+// route_split_sum_x16 (T <= 64 kDirectGroups, where one lane per token would leave most of
+// the chip idle): one block per 16 tokens (a quarter of a 64-token group), 16 lanes per token.
+// Lane sl of token r sums elements 4 sl .. 4 sl + 3 of the token's four partial rows in order,
+// ((P0 + P1) + P2) + P3 -- the logits, the same sums as above -- and the token is routed by
+// the 16-lane routing (route_token_x16, the same bits as the lane kernels).  The block's
+// per-expert assignment counts go to histogram (blockIdx.x % 4), column blockIdx.x / 4; the
+// grid has 4 blocks per group, so blocks past T write zero counts.
+template <int KMAX>
+__global__ __launch_bounds__(256) void route_split_sum_x16(const float* __restrict__ part,
+                                                           int64_t T, int K, float eps,
+                                                           int mode, int renorm, XTable xt,
+                                                           float* __restrict__ logits,
+                                                           int* __restrict__ kout,
+                                                           int* __restrict__ ids,
+                                                           float* __restrict__ wout,
+                                                           int* __restrict__ hist,
+                                                           int64_t hist_ld) {
+    __shared__ float rows[16][65];
+    __shared__ int h[64];
+    const int tr = threadIdx.x >> 4, sl = threadIdx.x & 15;
+    const int64_t t = (int64_t)blockIdx.x * 16 + tr;
+    const bool valid = t < T;
+    if (threadIdx.x < 64) h[threadIdx.x] = 0;
+    float4 v[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+        v[q] = valid ? *reinterpret_cast<const float4*>(part + ((int64_t)q * T + t) * 64 + 4 * sl)
+                     : make_float4(0.f, 0.f, 0.f, 0.f);  // rows past T: finite, never stored
+    const float l0 = ((v[0].x + v[1].x) + v[2].x) + v[3].x;
+    const float l1 = ((v[0].y + v[1].y) + v[2].y) + v[3].y;
+    const float l2 = ((v[0].z + v[1].z) + v[2].z) + v[3].z;
+    const float l3 = ((v[0].w + v[1].w) + v[2].w) + v[3].w;
+    if (logits && valid) {
+        float* const lt = logits + t * 64 + 4 * sl;
+        lt[0] = l0;
+        lt[1] = l1;
+        lt[2] = l2;
+        lt[3] = l3;
+    }
+    float* const row = &rows[tr][0];
+    row[4 * sl + 0] = l0;
+    row[4 * sl + 1] = l1;
+    row[4 * sl + 2] = l2;
+    row[4 * sl + 3] = l3;
+    __syncthreads();  // h zeroed (and the rows written) before any count
+    route_token_x16<KMAX>(row, K, eps, mode, renorm, xt, t, valid, kout, ids, wout, h);
+    __syncthreads();
+    if (threadIdx.x < 64)
+        hist[(int64_t)(blockIdx.x & 3) * 64 * hist_ld + (int64_t)threadIdx.x * hist_ld +
+             (blockIdx.x >> 2)] = h[threadIdx.x];
+}
+
 __global__ __launch_bounds__(256) void router_f32(const float* __restrict__ x,
                                                   const float* __restrict__ Wr, int64_t T,
                                                   int d, int N, float* __restrict__ logits) {
@@ -421,13 +473,23 @@ hipError_t launch_router_split_route(const void* x, const void* Wr, int64_t T, i
                            (const bf16_t*)x, (const bf16_t*)Wr, T, d, part);
     }
     ProfileScope prof("route_split_sum", s);
+    const XTable xt = make_xtable(64);
+    if (split_hist_subs(T) == kHistSubs) {  // 16 tokens per block, kHistSubs histograms
+        const dim3 grid(groups * kHistSubs);
+        if (p.K <= 8)
+            ELB_LAUNCH(route_split_sum_x16<8>, grid, dim3(256), 0, s, part, T, p.K, p.eps,
+                       p.mode, p.renormalize, xt, logits, k, ids, w, hist, hist_ld);
+        else
+            ELB_LAUNCH(route_split_sum_x16<kLaneMaxK>, grid, dim3(256), 0, s, part, T, p.K,
+                       p.eps, p.mode, p.renormalize, xt, logits, k, ids, w, hist, hist_ld);
+        return hipGetLastError();
+    }
     if (p.K <= 8)
         ELB_LAUNCH(route_split_sum<8>, dim3(groups), dim3(64), 0, s, part, T, p.K, p.eps,
-                   p.mode, p.renormalize, make_xtable(64), logits, k, ids, w, hist, hist_ld);
+                   p.mode, p.renormalize, xt, logits, k, ids, w, hist, hist_ld);
     else
         ELB_LAUNCH(route_split_sum<kLaneMaxK>, dim3(groups), dim3(64), 0, s, part, T, p.K,
-                   p.eps, p.mode, p.renormalize, make_xtable(64), logits, k, ids, w, hist,
-                   hist_ld);
+                   p.eps, p.mode, p.renormalize, xt, logits, k, ids, w, hist, hist_ld);
     return hipGetLastError();
 }
 

@@ -58,14 +58,18 @@ def test_fused_vs_oracle_olmoe():
 
 @pytest.mark.parametrize("T,d,K,mode", [(4096, 2048, 8, B.MODE_ELBOW), (1025, 512, 8, B.MODE_ELBOW),
                                         (4097, 512, 8, B.MODE_TOPK), (2048, 256, 16, B.MODE_ELBOW),
-                                        (8256, 1024, 12, B.MODE_ELBOW), (3000, 768, 8, B.MODE_ELBOW)])
+                                        (8256, 1024, 12, B.MODE_ELBOW), (3000, 768, 8, B.MODE_ELBOW),
+                                        (8192, 512, 8, B.MODE_ELBOW), (8193, 256, 16, B.MODE_TOPK)])
 def test_layer_split_router_equals_fused(T, d, K, mode):
     """Large batches with N = 64 and d % 256 == 0: the layer computes the router in four blocks
     per 64 tokens (each a quarter of the contraction) and routes in a second launch, which
     also writes the dispatch histogram.  Its logits, k, ids and w must be the one-block fused
-    kernel's bits (slices of 1, 2, 3, 4 and 8 64-column chunks; ragged T; T = 8256 takes the
-    dispatch's scan launch), its per-expert counts those of its routing, and its outputs the
-    oracle's."""
+    kernel's bits (slices of 1, 2, 3, 4 and 8 64-column chunks; ragged T).  Up to T = 8192 the
+    routing runs 16 tokens per block and writes one histogram per quarter of each 64-token
+    group, which the dispatch adds up; from T = 8193 (and T = 8256) one lane per token with one
+    histogram and the dispatch's scan launch.  Its per-expert counts must be those of its
+    routing, its output the bits of the expert stage run on the same routing (which counts the
+    assignments itself), and the oracle's."""
     L = synth.moe_layer(T, d, 64, 128, dtype="bf16", seed=T + d)
     x, Wr, Wgu, Wd = (to_gpu(a, BF) for a in (L.x, L.W_router, L.W_gu, L.W_down))
     y, dbg = B.elb_moe_forward(x, Wr, Wgu, Wd, K=K, mode=mode, debug=True)
@@ -76,6 +80,9 @@ def test_layer_split_router_equals_fused(T, d, K, mode):
     kk, ii = cpu(k), cpu(ids)
     assert np.array_equal(cpu(dbg["counts"]), np.bincount(ii[ii >= 0], minlength=64))
     assert cpu(dbg["counts"]).sum() == kk.sum()
+    y2 = B.elb_moe_experts(x, Wgu, Wd, k, ids, w)
+    torch.cuda.synchronize()
+    assert torch.equal(y, y2)
     tok = np.sort(np.random.default_rng(T).choice(T, 256, replace=False))
     ref = O.moe_experts(L.x, L.W_gu, L.W_down, kk[tok], ii[tok],
                         cpu(w)[tok].astype(np.float64), tokens=tok)
