@@ -56,11 +56,13 @@ hipError_t launch_route_pair(const float* logits, const float* rand, int64_t T, 
 inline int64_t dispatch_groups(int64_t T) { return (T + kWave - 1) / kWave; }
 inline int64_t dispatch_hist_ld(int64_t T) { return (dispatch_groups(T) + 3) & ~(int64_t)3; }
 inline int64_t dispatch_hist_ints(int64_t T, int N) { return dispatch_hist_ld(T) * N; }
-// up to this many groups the scatter sums the histogram itself (no scan launch)
+// up to this many groups the scatter sums the histogram itself (no scan launch); the
+// histogram is then group-major ([hist_ld, N]: row g holds the N counts of group g), else
+// expert-major ([N, hist_ld]) for the scan
 constexpr int64_t kDirectGroups = 128;
 // the split router's routing for T <= 64 kDirectGroups runs 16 tokens per block and writes
-// one histogram per quarter of each 64-token group: kHistSubs histograms [N, hist_ld], one
-// after the other, which the scatter adds up
+// one group-major histogram per quarter of each 64-token group: kHistSubs histograms of
+// hist_ld x N ints, one after the other, which the scatter adds up
 constexpr int kHistSubs = 4;
 inline int split_hist_subs(int64_t T) {
     return dispatch_groups(T) <= kDirectGroups ? kHistSubs : 1;
@@ -80,7 +82,8 @@ struct TilePlan {
 constexpr int kTailMax = 16;   // most experts whose remainders go to the tail kernel
 constexpr int kTailRows = 32;  // largest remainder the tail kernel takes
 
-// hist: dispatch_hist_ints(T, N) int32 scratch ([N, dispatch_hist_ld(T)], expert-major);
+// hist: dispatch_hist_ints(T, N) int32 scratch (group-major up to kDirectGroups groups,
+// else expert-major);
 // tile_off [N + 1]; tail_list [kTailMax + 1]
 // hist_ready: hist already holds the per-group counts (written by the split router), so the
 // count launch is skipped; hist_subs: how many histograms it holds (split_hist_subs(T) from

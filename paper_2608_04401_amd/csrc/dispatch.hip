@@ -4,7 +4,8 @@
 //   count   one lane per token; a wave ORs each token's selected experts into a 64-bit mask
 //           and, per expert, counts the wave's tokens with one ballot + popcount.  The
 //           per-wave counts form an expert-major [N, groups] histogram (row stride ld, a
-//           multiple of 4).
+//           multiple of 4), or a group-major one (row g: the N counts of group g) when the
+//           scatter reads it itself.
 //   scan    one block per expert: an exclusive prefix over groups (the base of each group
 //           inside the expert's list) and the expert's total.
 //   scatter one block of 4 waves per 64-token group, one lane per token.  Each wave forms
@@ -14,8 +15,9 @@
 //           lane, and its row is offsets[e] + base[e, group] + rank (each wave takes a quarter
 //           of the experts).  Rows within an expert are therefore in increasing token order.
 // Up to kDirectGroups groups (T <= 8192) the scan launch is skipped: every scatter wave reads
-// its experts' whole histogram rows (lane e: row e, 16-byte loads all in flight at once) and
-// forms the expert totals and its own group's base itself.  When the split router's routing
+// the whole group-major histogram (lane e: entry e of every group's row, so that each load is
+// one contiguous row; all in flight at once) and forms the expert totals and its own group's
+// base itself.  When the split router's routing
 // wrote one histogram per quarter of each group (kHistSubs of them), wave w reads histogram w
 // and the four waves add their sums through LDS.  One launch (dispatch_small) for T <= 256.
 // All three forms give the same rows.
@@ -35,6 +37,31 @@ __device__ __forceinline__ void load_ids8(const int* __restrict__ ids, int64_t t
                                           int (&e8)[8]) {
 #pragma unroll
     for (int q = 0; q < 8; ++q) e8[q] = (j0 + q < K) ? ids[t * K + j0 + q] : -1;
+}
+
+// the mask of token t's first kt experts from its slots: the first eight already loaded
+// (e8), the rest (K > 8) loaded here
+__device__ __forceinline__ uint64_t token_mask_pre(int kt, const int (&e8)[8],
+                                                   const int* __restrict__ ids, int64_t t,
+                                                   int N, int K, bool valid) {
+    uint64_t mask = 0;
+    if (valid) {
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+            const int e = e8[q];
+            if (q < kt && (unsigned)e < (unsigned)N) mask |= 1ull << e;
+        }
+        for (int j0 = 8; j0 < K; j0 += 8) {
+            int f8[8];
+            load_ids8(ids, t, K, j0, f8);
+#pragma unroll
+            for (int q = 0; q < 8; ++q) {
+                const int e = f8[q];
+                if (j0 + q < kt && (unsigned)e < (unsigned)N) mask |= 1ull << e;
+            }
+        }
+    }
+    return mask;
 }
 
 __device__ __forceinline__ uint64_t token_mask(const int* __restrict__ k,
@@ -87,9 +114,11 @@ __device__ __forceinline__ void write_tail_list(bool tail_mine, int n_tail, int 
     if (lane == 0) tail_list[0] = n_tail;
 }
 
+// gmajor: write the group-major histogram the scatter reads itself (row g of N counts), else
+// the expert-major one the scan launch takes
 __global__ __launch_bounds__(64 * kDispWaves) void dispatch_count(
     const int* __restrict__ k, const int* __restrict__ ids, int64_t T, int N, int K, int64_t ld,
-    int* __restrict__ hist) {
+    int gmajor, int* __restrict__ hist) {
     const int lane = threadIdx.x & (kWave - 1);
     const int64_t g = (int64_t)blockIdx.x * kDispWaves + (threadIdx.x >> 6);
     const int64_t t = g * kWave + lane;
@@ -102,7 +131,7 @@ __global__ __launch_bounds__(64 * kDispWaves) void dispatch_count(
         const int c = __popcll(b);
         if (lane == e) mine = c;
     }
-    if (lane < N) hist[(int64_t)lane * ld + g] = mine;
+    if (lane < N) hist[gmajor ? g * N + lane : (int64_t)lane * ld + g] = mine;
 }
 
 // one block per expert e: exclusive prefix of hist[e, :] over the groups, in place
@@ -159,10 +188,24 @@ __global__ __launch_bounds__(64 * kScatterWaves) void dispatch_scatter(
     __shared__ int pos[kWave][kWave + 1];  // [token lane][expert]: the token's row
     __shared__ int red[2][kScatterWaves][kWave];  // per-wave sums of the sub-histograms
     const int lane = threadIdx.x & (kWave - 1);
-    const int wv = threadIdx.x >> 6;
+    const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave-uniform
     const int64_t g = blockIdx.x;
     const int64_t t = g * kWave + lane;
     const int64_t groups = (T + kWave - 1) / kWave;
+    // the lane's token: k and its first eight slots, loaded before the histogram (both in
+    // flight together) and kept for the inverse map.  No per-lane branch around the loads (a
+    // lane past T reads token T - 1 and drops it): behind a divergent branch the compiler
+    // cannot tell the loads have landed and waits for every memory operation, the row stores
+    // below included, before each later use.
+    const bool valid = t < T;  // false for every lane of a block past the groups (T == 0)
+    int kt = 0, e8[8];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) e8[q] = -1;
+    if (T > 0) {  // uniform
+        const int64_t tc = valid ? t : T - 1;
+        kt = valid ? k[tc] : 0;
+        load_ids8(ids, tc, K, 0, e8);
+    }
     // expert list offsets and M-tile offsets: exclusive prefixes over the experts (lane e),
     // formed by every wave.  c: expert e's total; hist_mine: the base of this group inside
     // expert e's list.
@@ -171,27 +214,21 @@ __global__ __launch_bounds__(64 * kScatterWaves) void dispatch_scatter(
         // lane e sums row e of the raw histogram: all of it (the total) and the groups below
         // g (the base), in group order; pads past `groups` are not read as counts
         const int sub = subs > 1 ? wv : 0;  // wave wv reads histogram wv (or the only one)
-        if (lane < N) {
-            const int4* h4 =
-                reinterpret_cast<const int4*>(hist + sub * sub_stride + (int64_t)lane * ld);
-            const int n4 = (int)(ld >> 2), ng = (int)groups, gg = (int)g;
-            int4 v[kDirectGroups / 4];
+        {
+            // group-major: lane e reads entry e of every group's row (each load one contiguous
+            // row of N counts); lanes past N read entry N - 1 and drop it (no per-lane branch
+            // around the loads)
+            const int* const hb = hist + sub * sub_stride + (lane < N ? lane : N - 1);
+            const int ng = (int)groups, gg = (int)g;
+            int v[kDirectGroups];
 #pragma unroll
-            for (int q = 0; q < kDirectGroups / 4; ++q) {
-                v[q] = make_int4(0, 0, 0, 0);
-                if (q < n4) v[q] = h4[q];
+            for (int q = 0; q < kDirectGroups; ++q) v[q] = (q < ng) ? hb[(int64_t)q * N] : 0;
+#pragma unroll
+            for (int q = 0; q < kDirectGroups; ++q) {
+                c += v[q];
+                hist_mine += q < gg ? v[q] : 0;
             }
-#pragma unroll
-            for (int q = 0; q < kDirectGroups / 4; ++q) {
-#pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    const int gi = 4 * q + r;
-                    const int x0 = r == 0 ? v[q].x : r == 1 ? v[q].y : r == 2 ? v[q].z : v[q].w;
-                    const int x = gi < ng ? x0 : 0;
-                    c += x;
-                    hist_mine += gi < gg ? x : 0;
-                }
-            }
+            if (lane >= N) c = hist_mine = 0;
         }
         if (subs > 1) {  // block-uniform: every wave takes the sums over the histograms
             red[0][wv][lane] = c;
@@ -237,8 +274,7 @@ __global__ __launch_bounds__(64 * kScatterWaves) void dispatch_scatter(
         write_tail_list(tail_mine, n_tail, lane, tail_list);
     }
     if (g >= groups) return;  // block-uniform (T == 0: the one block only writes the offsets)
-    const bool valid = t < T;
-    const uint64_t mask = token_mask(k, ids, t, N, K, valid);
+    const uint64_t mask = token_mask_pre(kt, e8, ids, t, N, K, valid);
     // lane e holds the first row of expert e that belongs to this group
     const int base_mine = (lane < N) ? off_mine + hist_mine : 0;
     const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
@@ -256,8 +292,16 @@ __global__ __launch_bounds__(64 * kScatterWaves) void dispatch_scatter(
     }
     __syncthreads();
     if (!valid) return;  // no barrier follows
-    const int kt = k[t];
-    for (int j = wv; j < K; j += kScatterWaves) {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+        if (j < K && j % kScatterWaves == wv) {  // wave-uniform
+            const int e = e8[j];
+            int r = -1;
+            if (j < kt && (unsigned)e < (unsigned)N) r = pos[lane][e];
+            inv[t * K + j] = r;
+        }
+    }
+    for (int j = 8 + wv; j < K; j += kScatterWaves) {
         const int e = ids[t * K + j];
         int r = -1;
         if (j < kt && (unsigned)e < (unsigned)N) r = pos[lane][e];
@@ -379,7 +423,7 @@ hipError_t launch_dispatch(const int* k, const int* ids, int64_t T, int N, int K
     if (T > 0 && !hist_ready) {
         ProfileScope prof("dispatch_count", s);
         ELB_LAUNCH(dispatch_count, dim3(blocks), dim3(64 * kDispWaves), 0, s, k, ids, T,
-                           N, K, ld, hist);
+                           N, K, ld, (int)direct, hist);
     }
     if (!direct) {
         ProfileScope prof("dispatch_scan", s);
