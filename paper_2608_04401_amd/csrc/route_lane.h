@@ -357,10 +357,46 @@ __device__ __forceinline__ void route_token(const float* row, int N, int K, floa
 // the order-preserving integer image of a canonical fp32 value, and its inverse
 __device__ __forceinline__ int ord_flip32(int i) { return i ^ ((i >> 31) & 0x7fffffff); }
 
-__device__ __forceinline__ int64_t shfl_xor64(int64_t v, int m) {
-    const int lo = __shfl_xor((int)(uint32_t)v, m, 16);
-    const int hi = __shfl_xor((int)(v >> 32), m, 16);
+// The value of lane l ^ M (M = 1, 2, 4, 8) inside each 16-lane row, by DPP: a modifier of one
+// VALU move, with no LDS round trip (a ds_bpermute costs one, and the 16-lane routing's
+// exchanges form a dependent chain).  M = 1, 2: quad permutations; M = 8: rotation of the row
+// by 8; M = 4: rotations by 4 and by 12, chosen by lane bit 2 (lane l takes lane (l - 4)
+// mod 16 or (l - 12) mod 16, whichever is l ^ 4).
+template <int M>
+__device__ __forceinline__ int xor16(int v) {
+    static_assert(M == 1 || M == 2 || M == 4 || M == 8, "row exchange");
+    if constexpr (M == 1) return __builtin_amdgcn_update_dpp(0, v, 0xB1, 0xF, 0xF, false);
+    else if constexpr (M == 2) return __builtin_amdgcn_update_dpp(0, v, 0x4E, 0xF, 0xF, false);
+    else if constexpr (M == 8) return __builtin_amdgcn_update_dpp(0, v, 0x128, 0xF, 0xF, false);
+    else {
+        const int r4 = __builtin_amdgcn_update_dpp(0, v, 0x124, 0xF, 0xF, false);
+        const int r12 = __builtin_amdgcn_update_dpp(0, v, 0x12C, 0xF, 0xF, false);
+        return (threadIdx.x & 4) ? r4 : r12;
+    }
+}
+template <int M>
+__device__ __forceinline__ float xor16f(float v) { return __int_as_float(xor16<M>(__float_as_int(v))); }
+template <int M>
+__device__ __forceinline__ int64_t xor16_64(int64_t v) {
+    const int lo = xor16<M>((int)(uint32_t)v);
+    const int hi = xor16<M>((int)(v >> 32));
     return ((int64_t)hi << 32) | (uint32_t)lo;
+}
+__device__ __forceinline__ int64_t xor16_64(int64_t v, int m) {  // m a constant after unrolling
+    switch (m) {
+        case 1: return xor16_64<1>(v);
+        case 2: return xor16_64<2>(v);
+        case 4: return xor16_64<4>(v);
+        default: return xor16_64<8>(v);
+    }
+}
+// lane 0 (first) or lane 15 (last) of each 16-lane row, by a swizzle (bit mode: lane & 0x10,
+// or 0x0f)
+__device__ __forceinline__ float row_first(float v) {
+    return __int_as_float(__builtin_amdgcn_ds_swizzle(__float_as_int(v), 0x10));
+}
+__device__ __forceinline__ float row_last(float v) {
+    return __int_as_float(__builtin_amdgcn_ds_swizzle(__float_as_int(v), 0x10 | (0x0f << 5)));
 }
 
 // row: the token's 64 logits in LDS; every lane of the group calls this (valid: the token
@@ -394,7 +430,7 @@ __device__ __forceinline__ void route_token_x16(float* row, int K, float eps, in
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
                     const int p = 4 * sl + i;
-                    const int64_t w = shfl_xor64(v[i], m);
+                    const int64_t w = xor16_64(v[i], m);
                     const bool desc = (p & k) == 0 || k == NP;
                     const bool lower = (p & j) == 0;
                     const bool take_max = lower == desc;
@@ -422,15 +458,17 @@ __device__ __forceinline__ void route_token_x16(float* row, int K, float eps, in
         key[i] = __int_as_float(ord_flip32((int)(v[i] >> 32)));
         id[i] = NP - 1 - (int)(uint32_t)v[i];
     }
-    const float nl = neg_scaled(__shfl(key[0], 0, 16));
+    const float nl = neg_scaled(row_first(key[0]));
     float u[4];
 #pragma unroll
     for (int i = 0; i < 4; ++i) u[i] = rel_exp(key[i], nl);
     // ---- S over the ranks (tree_sum by a butterfly), u_min = u of rank 63 ----
     float S = (u[0] + u[1]) + (u[2] + u[3]);
-#pragma unroll
-    for (int m = 1; m < 16; m <<= 1) S += __shfl_xor(S, m, 16);
-    const float umin = __shfl(u[3], 15, 16);
+    S += xor16f<1>(S);
+    S += xor16f<2>(S);
+    S += xor16f<4>(S);
+    S += xor16f<8>(S);
+    const float umin = row_last(u[3]);
     int k = K;
     if (mode == ELB_MODE_ELBOW) {
         const float Rp = (1.0f - umin) + eps * S;
@@ -451,17 +489,17 @@ __device__ __forceinline__ void route_token_x16(float* row, int K, float eps, in
                 tail = fminf(tail, Ei);
             }
         }
-#pragma unroll
-        for (int m = 8; m >= 1; m >>= 1) {
-            const float obd = __shfl_xor(bd, m, 16);
-            const int obe = __shfl_xor(be, m, 16);
-            const float ot = __shfl_xor(tail, m, 16);
+        auto step = [&](float obd, int obe, float ot) {
             if (obd < bd || (obd == bd && obe < be)) {
                 bd = obd;
                 be = obe;
             }
             tail = fminf(tail, ot);
-        }
+        };
+        step(xor16f<8>(bd), xor16<8>(be), xor16f<8>(tail));
+        step(xor16f<4>(bd), xor16<4>(be), xor16f<4>(tail));
+        step(xor16f<2>(bd), xor16<2>(be), xor16f<2>(tail));
+        step(xor16f<1>(bd), xor16<1>(be), xor16f<1>(tail));
         k = (tail < bd) ? K : be + 1;
     }
     float denom = S;
@@ -470,8 +508,10 @@ __device__ __forceinline__ void route_token_x16(float* row, int K, float eps, in
 #pragma unroll
         for (int i = 0; i < 4; ++i) m4[i] = (4 * sl + i < k) ? u[i] : 0.f;
         denom = (m4[0] + m4[1]) + (m4[2] + m4[3]);
-#pragma unroll
-        for (int m = 1; m < 16; m <<= 1) denom += __shfl_xor(denom, m, 16);
+        denom += xor16f<1>(denom);
+        denom += xor16f<2>(denom);
+        denom += xor16f<4>(denom);
+        denom += xor16f<8>(denom);
     }
     const float inv = 1.0f / denom;
     if (!valid) return;
