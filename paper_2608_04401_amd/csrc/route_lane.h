@@ -74,7 +74,7 @@ __device__ __forceinline__ void sort_desc(float* key, std::integer_sequence<int,
 // kernel sums S (and a renormalised denominator) over the ranks in this one order, so that
 // all of them give the same bits: a lane that holds all n values adds them in this tree, and
 // lanes holding 4 consecutive ranks each add their 4 as (v0 + v1) + (v2 + v3) and then
-// combine with a butterfly (shfl_xor 1, 2, 4, ...), which walks the same tree (IEEE addition
+// combine with an XOR butterfly (partners 1, 2, 4, 8), which walks the same tree (IEEE addition
 // is commutative, and adding the exact zeros of masked ranks changes nothing).
 template <int n>
 __device__ __forceinline__ float tree_sum(const float* v) {
@@ -347,12 +347,12 @@ __device__ __forceinline__ void route_token(const float* row, int N, int K, floa
 
 // ---- one token by 16 lanes (N = 64): for latency, where few tokens are routed at once ----
 //
-// The same keys, u, S, deviations, first argmax and weights as route_token, bit for bit, with
-// the work spread over 16 consecutive lanes of a wave (lane sl holds ranks 4 sl .. 4 sl + 3):
-// the (key, id) pairs are sorted by a bitonic network whose strides of 4 and more cross lanes
-// (shuffles inside the 16-lane group); S (and the renormalised denominator) is summed in rank
-// order by the group's first lane from the u values left in the token's LDS row; the first
-// argmax and the tail maximum are exact reductions over the group.
+// The same keys, u, S, deviations, first argmin and weights as route_token, bit for bit, with
+// the work spread over 16 consecutive lanes of a wave, one 16-lane DPP row (lane sl holds
+// ranks 4 sl .. 4 sl + 3): the (key, id) pairs are sorted by a bitonic network whose strides
+// of 4 and more cross lanes (row exchanges by DPP); S (and the renormalised denominator) is
+// the tree_sum order walked by an XOR butterfly; the first argmin of E and the tail minimum
+// are exact reductions over the row.
 
 // the order-preserving integer image of a canonical fp32 value, and its inverse
 __device__ __forceinline__ int ord_flip32(int i) { return i ^ ((i >> 31) & 0x7fffffff); }
