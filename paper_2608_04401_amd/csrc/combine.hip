@@ -4,7 +4,9 @@
 // summed in rank order j = 0, 1, ... with fp32 accumulation (deterministic; no atomics).
 // y may alias residual (each element is read, then written, by the same thread).
 // One block per token; each thread owns 8 (bf16) or 4 (fp32) consecutive columns, so every
-// expert row is read with 16-byte coalesced loads.
+// expert row is read with 16-byte coalesced loads.  The token's slots are taken eight at a
+// time: their rows and weights first, then all eight row loads at once, then the FMAs in rank
+// order, so a block waits for memory once per eight experts instead of twice per expert.
 #include "common.h"
 
 namespace elb {
@@ -18,7 +20,7 @@ __global__ __launch_bounds__(256) void combine_bf16(const bf16_t* __restrict__ Y
                                                     const bf16_t* residual,
                                                     int64_t T, int d, int K, bf16_t* y) {
     const int64_t t = blockIdx.x;
-    const int kt = k[t];
+    const int kt = k[t] < K ? k[t] : K;  // block-uniform
     for (int c = threadIdx.x * 8; c < d; c += 256 * 8) {
         float acc[8];
         if (residual) {
@@ -30,14 +32,31 @@ __global__ __launch_bounds__(256) void combine_bf16(const bf16_t* __restrict__ Y
 #pragma unroll
             for (int i = 0; i < 8; ++i) acc[i] = 0.f;
         }
-        for (int j = 0; j < kt && j < K; ++j) {
-            const int64_t r = inv ? inv[t * K + j] : t * K + j;
-            if (r < 0) continue;
-            const float wj = w[t * K + j];
-            const uint4 q = *reinterpret_cast<const uint4*>(Y + r * d + c);
-            const bf16_t* h = reinterpret_cast<const bf16_t*>(&q);
+        for (int j0 = 0; j0 < kt; j0 += 8) {
+            int64_t r[8];
+            float wj[8];
 #pragma unroll
-            for (int i = 0; i < 8; ++i) acc[i] = fmaf(wj, bf16_to_f32(h[i]), acc[i]);
+            for (int q = 0; q < 8; ++q) {
+                const int j = j0 + q;
+                r[q] = -1;
+                wj[q] = 0.f;
+                if (j < kt) {
+                    r[q] = inv ? inv[t * K + j] : t * K + j;
+                    wj[q] = w[t * K + j];
+                }
+            }
+            uint4 yq[8];
+#pragma unroll
+            for (int q = 0; q < 8; ++q)
+                yq[q] = r[q] >= 0 ? *reinterpret_cast<const uint4*>(Y + r[q] * d + c)
+                                  : make_uint4(0u, 0u, 0u, 0u);
+#pragma unroll
+            for (int q = 0; q < 8; ++q) {
+                if (r[q] < 0) continue;  // slots past k_t, and dropped ones, add nothing
+                const bf16_t* h = reinterpret_cast<const bf16_t*>(&yq[q]);
+#pragma unroll
+                for (int i = 0; i < 8; ++i) acc[i] = fmaf(wj[q], bf16_to_f32(h[i]), acc[i]);
+            }
         }
         uint4 o;
         bf16_t* ob = reinterpret_cast<bf16_t*>(&o);
@@ -54,19 +73,36 @@ __global__ __launch_bounds__(256) void combine_f32(const float* __restrict__ Y,
                                                    const float* residual,
                                                    int64_t T, int d, int K, float* y) {
     const int64_t t = blockIdx.x;
-    const int kt = k[t];
+    const int kt = k[t] < K ? k[t] : K;  // block-uniform
     for (int c = threadIdx.x * 4; c < d; c += 256 * 4) {
         float4 acc = residual ? *reinterpret_cast<const float4*>(residual + t * d + c)
                               : make_float4(0.f, 0.f, 0.f, 0.f);
-        for (int j = 0; j < kt && j < K; ++j) {
-            const int64_t r = inv ? inv[t * K + j] : t * K + j;
-            if (r < 0) continue;
-            const float wj = w[t * K + j];
-            const float4 q = *reinterpret_cast<const float4*>(Y + r * d + c);
-            acc.x = fmaf(wj, q.x, acc.x);
-            acc.y = fmaf(wj, q.y, acc.y);
-            acc.z = fmaf(wj, q.z, acc.z);
-            acc.w = fmaf(wj, q.w, acc.w);
+        for (int j0 = 0; j0 < kt; j0 += 8) {
+            int64_t r[8];
+            float wj[8];
+#pragma unroll
+            for (int q = 0; q < 8; ++q) {
+                const int j = j0 + q;
+                r[q] = -1;
+                wj[q] = 0.f;
+                if (j < kt) {
+                    r[q] = inv ? inv[t * K + j] : t * K + j;
+                    wj[q] = w[t * K + j];
+                }
+            }
+            float4 yq[8];
+#pragma unroll
+            for (int q = 0; q < 8; ++q)
+                yq[q] = r[q] >= 0 ? *reinterpret_cast<const float4*>(Y + r[q] * d + c)
+                                  : make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+            for (int q = 0; q < 8; ++q) {
+                if (r[q] < 0) continue;
+                acc.x = fmaf(wj[q], yq[q].x, acc.x);
+                acc.y = fmaf(wj[q], yq[q].y, acc.y);
+                acc.z = fmaf(wj[q], yq[q].z, acc.z);
+                acc.w = fmaf(wj[q], yq[q].w, acc.w);
+            }
         }
         *reinterpret_cast<float4*>(y + t * d + c) = acc;
     }
