@@ -571,7 +571,21 @@ def calibration(B, torch):
     gbs = 2 * a.numel() * 4 * 10 / (e0.elapsed_time(e1) * 1e-3) / 1e9
     out["hbm_copy"] = {"what": "1 GiB device-to-device copy (read + write bytes)",
                        "GB/s": round(gbs, 1), "frac_of_spec": round(gbs / PEAK_HBM_GBS, 4)}
-    del a, b
+    # read-only stream over the same 1 GiB (more than the 256 MB last-level cache): the rate
+    # for read-dominated kernels (decode weight streams, the combine)
+    wv = torch.empty(4096 * 4, dtype=torch.int32, device="cuda")
+    B.elb_calibrate_read_stream(a, 4096, wv)
+    torch.cuda.synchronize()
+    e0.record()
+    for _ in range(10):
+        B.elb_calibrate_read_stream(a, 4096, wv)
+    e1.record()
+    torch.cuda.synchronize()
+    rbs = a.numel() * 4 * 10 / (e0.elapsed_time(e1) * 1e-3) / 1e9
+    out["hbm_read_stream"] = {"what": "1 GiB read once per call (library calibration kernel, "
+                                      "4096 blocks, non-temporal 16-byte loads)",
+                              "GB/s": round(rbs, 1), "frac_of_spec": round(rbs / PEAK_HBM_GBS, 4)}
+    del a, b, wv
     blocks, iters = 1024, 4000
     B.elb_calibrate_mfma_bf16(blocks, 50)
     torch.cuda.synchronize()

@@ -282,6 +282,20 @@ int elb_moe_forward_packed(const void *x, const void *W_router, const void *W_ga
 int64_t elb_calibrate_mfma_bf16(int32_t blocks, int32_t iters, float *out, void *stream);
 
 /*
+ * Calibration of the HBM read roofline (a measurement aid, not part of the layer): `blocks`
+ * blocks of 4 waves read the whole of buf once, each block its own contiguous share, with
+ * coalesced non-temporal 16-byte loads (sixteen in flight per lane), and fold the words into
+ * one per wave.
+ * Timing it over a buffer larger than the last-level cache gives the read rate the chip
+ * sustains.
+ *   buf   [bytes] device memory, 16-byte aligned; bytes a positive multiple of 16 (read only)
+ *   out   [blocks * 4] uint32 device output (one word per wave, so the reads are kept)
+ * Returns ELB_OK or an elb_status; nothing is allocated.
+ */
+int elb_calibrate_read_stream(const void *buf, int64_t bytes, int32_t blocks, uint32_t *out,
+                              void *stream);
+
+/*
  * Per-kernel timing (hipEvents attached to each launch the library makes).
  * elb_profile_enable(1) starts recording on the calling process for every launch,
  * elb_profile_enable(2) for the grouped expert GEMMs only, elb_profile_enable(0) stops; a

@@ -72,6 +72,7 @@ def lib():
         "elb_moe_forward_noalloc": ([P, P, P, P, P, I64, I32, I32, I32, I32,
                                      C.POINTER(RouteParams), P, P, P, P, P, P, P], C.c_int),
         "elb_calibrate_mfma_bf16": ([I32, I32, P, P], C.c_int64),
+        "elb_calibrate_read_stream": ([P, I64, I32, P, P], C.c_int),
         "elb_profile_enable": ([C.c_int], C.c_int),
         "elb_profile_read": ([C.POINTER(C.c_char_p), C.POINTER(C.c_double),
                               C.POINTER(C.c_int64), C.c_int], C.c_int),
@@ -366,6 +367,13 @@ def elb_moe_forward_prepared(x, W_router, W_gate_up, W_down, K: int = 8, eps: fl
             _check(name, rc)
         return keep
     return call, y
+
+
+def elb_calibrate_read_stream(buf: torch.Tensor, blocks: int, out: torch.Tensor) -> None:
+    """Enqueue the read-only stream over the bytes of buf (out: blocks * 4 int32 words)."""
+    _dev(buf, out)
+    _check("elb_calibrate_read_stream", lib().elb_calibrate_read_stream(
+        _ptr(buf), buf.numel() * buf.element_size(), blocks, _ptr(out), _stream()))
 
 
 def elb_calibrate_mfma_bf16(blocks: int, iters: int) -> int:

@@ -582,6 +582,18 @@ int64_t elb_calibrate_mfma_bf16(int32_t blocks, int32_t iters, float* out, void*
     return (int64_t)blocks * 4 * iters * 8;
 }
 
+int elb_calibrate_read_stream(const void* buf, int64_t bytes, int32_t blocks, uint32_t* out,
+                              void* stream) {
+    g_err.clear();
+    if (!buf || !out) return fail(ELB_ERR_INVALID_ARG, "NULL tensor pointer");
+    if (bytes < 16 || bytes % 16 || (uintptr_t)buf % 16)
+        return fail(ELB_ERR_INVALID_ARG, "buffer of %lld bytes: need a positive multiple of 16, "
+                    "16-byte aligned", (long long)bytes);
+    if (blocks < 1) return fail(ELB_ERR_INVALID_ARG, "blocks = %d must be >= 1", blocks);
+    return hip_status(launch_calibrate_read(buf, bytes, blocks, out, (hipStream_t)stream),
+                      "calibrate_read");
+}
+
 int elb_profile_enable(int on) {
     if (on < 0 || on > 2) return fail(ELB_ERR_INVALID_ARG, "profiling level %d outside [0, 2]", on);
     g_prof_on.store(on);

@@ -7,6 +7,7 @@
 // expert row is read with 16-byte coalesced loads.  The token's slots are taken eight at a
 // time: their rows and weights first, then all eight row loads at once, then the FMAs in rank
 // order, so a block waits for memory once per eight experts instead of twice per expert.
+// (Plain loads: Y was just written by the down GEMM, and non-temporal loads measured slower.)
 #include "common.h"
 
 namespace elb {

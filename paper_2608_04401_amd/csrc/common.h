@@ -147,6 +147,8 @@ hipError_t launch_combine(const void* Y, const int* k, const int* inv, const flo
 
 // calibration: back-to-back bf16 MFMAs, blocks x 4 waves x iters x 8 of them; out [blocks * 4]
 hipError_t launch_calibrate_mfma(int blocks, int iters, float* out, hipStream_t s);
+hipError_t launch_calibrate_read(const void* buf, int64_t bytes, int blocks, uint32_t* out,
+                                 hipStream_t s);
 
 // ---- per-kernel timing hooks (api.hip) ----
 // A ProfileScope names the launches made while it is alive (on the calling thread).  With the

@@ -175,3 +175,16 @@ def test_noalloc_rejects_oversized_problems_on_the_host():
     assert lib.elb_moe_forward_noalloc(None, None, None, None, None, 0, 2048, 64, 1024,
                                        B.ELB_BF16, C.byref(p), None, None, None, None, None,
                                        None, None) == OK
+
+
+def test_read_stream_calibration_validates_on_the_host():
+    """The read-stream calibration rejects a NULL buffer, sizes that are not a positive
+    multiple of 16, a misaligned buffer and blocks < 1 before launching anything."""
+    lib = B.lib()
+    assert lib.elb_calibrate_read_stream(None, 1024, 4, DUMMY, None) == INVALID
+    assert lib.elb_calibrate_read_stream(DUMMY, 1024, 4, None, None) == INVALID
+    assert lib.elb_calibrate_read_stream(DUMMY, 0, 4, DUMMY, None) == INVALID
+    assert lib.elb_calibrate_read_stream(DUMMY, 1000, 4, DUMMY, None) == INVALID
+    assert lib.elb_calibrate_read_stream(C.c_void_p(DUMMY.value + 8), 1024, 4, DUMMY,
+                                         None) == INVALID
+    assert lib.elb_calibrate_read_stream(DUMMY, 1024, 0, DUMMY, None) == INVALID
