@@ -355,9 +355,10 @@ __global__ __launch_bounds__(64) void route_split_sum(const float* __restrict__ 
 // Lane sl of token r sums elements 4 sl .. 4 sl + 3 of the token's four partial rows in order,
 // ((P0 + P1) + P2) + P3 -- the logits, the same sums as above -- and the token is routed by
 // the 16-lane routing (route_token_x16, the same bits as the lane kernels).  The block's
-// per-expert assignment counts go to histogram (blockIdx.x % 4), row blockIdx.x / 4 (the
-// group-major layout the scatter reads: one contiguous row of 64 counts per group); the grid
-// has 4 blocks per group, so blocks past T write zero counts.
+// per-expert assignment counts go to histogram blockIdx.x % kHistSubs, row blockIdx.x /
+// kHistSubs (the group-major layout the scatter reads: one contiguous row of 64 counts per
+// group); the grid has kHistSubs blocks per group, so blocks past T write zero counts.
+static_assert(16 * kHistSubs == kWave, "four 16-token blocks per 64-token group");
 template <int KMAX>
 __global__ __launch_bounds__(256) void route_split_sum_x16(const float* __restrict__ part,
                                                            int64_t T, int K, float eps,
@@ -398,9 +399,10 @@ __global__ __launch_bounds__(256) void route_split_sum_x16(const float* __restri
     __syncthreads();  // h zeroed (and the rows written) before any count
     route_token_x16<KMAX>(row, K, eps, mode, renorm, xt, t, valid, kout, ids, wout, h);
     __syncthreads();
-    if (threadIdx.x < 64)
-        hist[((int64_t)(blockIdx.x & 3) * hist_ld + (blockIdx.x >> 2)) * 64 + threadIdx.x] =
-            h[threadIdx.x];
+    if (threadIdx.x < 64) {
+        const int64_t j = blockIdx.x % kHistSubs, g = blockIdx.x / kHistSubs;
+        hist[(j * hist_ld + g) * 64 + threadIdx.x] = h[threadIdx.x];
+    }
 }
 
 __global__ __launch_bounds__(256) void router_f32(const float* __restrict__ x,
