@@ -204,6 +204,7 @@ int elb_moe_experts(const void *x, const void *W_gate_up, const void *W_down,
  * skip) receive the intermediate results of this call:
  *   logits_out [T, N] float, k_out [T], ids_out [T, K], w_out [T, K],
  *   counts_out [N] int32 (assignments per expert).
+ * With T = 0 nothing is launched and no output (counts_out included) is written.
  */
 int elb_moe_forward(const void *x, const void *W_router, const void *W_gate_up,
                     const void *W_down, const void *residual, int64_t T, int32_t d, int32_t N,

@@ -271,3 +271,26 @@ def test_forward_residual_stack_two_layers():
         near = ref.routing.margin < NEAR_TIE
         assert rel[~near].max() < RTOL_BF16
         h = synth.round_bf16(ref.y.astype(np.float32))
+
+
+@pytest.mark.parametrize("dtype", [torch.float32, BF])
+def test_forward_and_experts_empty_batch(dtype):
+    """T = 0: the layer and the expert stage return at once with empty outputs (nothing is
+    launched), and the dispatch writes all-zero counts and offsets, for both dtypes."""
+    d, N, m, K = 128, 8, 64, 4
+    g = torch.Generator(device="cuda")
+    g.manual_seed(3)
+    x = torch.empty((0, d), dtype=dtype, device="cuda")
+    Wr = (torch.randn((N, d), generator=g, device="cuda") * 0.02).to(dtype)
+    Wgu = (torch.randn((N, 2 * m, d), generator=g, device="cuda") * 0.02).to(dtype)
+    Wd = (torch.randn((N, d, m), generator=g, device="cuda") * 0.02).to(dtype)
+    y, dbg = B.elb_moe_forward(x, Wr, Wgu, Wd, K=K, debug=True)
+    k = torch.empty(0, dtype=torch.int32, device="cuda")
+    ids = torch.empty((0, K), dtype=torch.int32, device="cuda")
+    w = torch.empty((0, K), dtype=torch.float32, device="cuda")
+    y2 = B.elb_moe_experts(x, Wgu, Wd, k, ids, w)
+    counts, offsets, row_token, inv = B.elb_dispatch(k, ids, N)
+    torch.cuda.synchronize()
+    assert y.shape == (0, d) and y2.shape == (0, d)
+    assert dbg["k"].numel() == 0 and dbg["ids"].shape == (0, K)
+    assert int(counts.abs().sum()) == 0 and int(offsets.abs().sum()) == 0
