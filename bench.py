@@ -805,7 +805,13 @@ def main():
             "hbm", us_of("router_bf16"), 2 * T * d + 2 * N * d + 4 * T * N, PEAK_HBM_GBS),
         "routing (softmax, sort, elbow, cap, weights)": row(
             "hbm", us_of("route"), 4 * T * N + T * (4 + 8 * K), PEAK_HBM_GBS),
-        # the layer's default for bf16: one kernel, logits kept on chip
+        # the layer's form for T > 1024 (N = 64, d % 256 = 0): quarter-contraction router
+        # blocks, then the sum, the routing and the dispatch histogram (partials not counted)
+        "router + routing (split form)": row(
+            "hbm", us_of("router_split_bf16") + us_of("route_split_sum"),
+            2 * T * d + 2 * N * d + T * (4 + 8 * K), PEAK_HBM_GBS)
+        if us_of("router_split_bf16") > 0 and us_of("route_split_sum") > 0 else None,
+        # the one-kernel form (other bf16 layers with K <= 16): logits kept on chip
         "router + routing fused": row(
             "hbm", us_of("router_route_bf16"), 2 * T * d + 2 * N * d + T * (4 + 8 * K),
             PEAK_HBM_GBS),
