@@ -17,10 +17,9 @@
 // Up to kDirectGroups groups (T <= 8192) the scan launch is skipped: every scatter wave reads
 // the whole group-major histogram (lane e: entry e of every group's row, so that each load is
 // one contiguous row; all in flight at once) and forms the expert totals and its own group's
-// base itself.  When the split router's routing
-// wrote one histogram per quarter of each group (kHistSubs of them), wave w reads histogram w
-// and the four waves add their sums through LDS.  One launch (dispatch_small) for T <= 256.
-// All three forms give the same rows.
+// base itself.  When the split router's routing wrote one histogram per quarter of each group
+// (kHistSubs of them), wave w reads histogram w and the four waves add their sums through
+// LDS.  One launch (dispatch_small) for T <= 256.  All three forms give the same rows.
 // Requires N <= 64 (one mask bit per expert).
 #include "common.h"
 
@@ -211,8 +210,9 @@ __global__ __launch_bounds__(64 * kScatterWaves) void dispatch_scatter(
     // expert e's list.
     int c = 0, hist_mine = 0;
     if (DIRECT) {
-        // lane e sums row e of the raw histogram: all of it (the total) and the groups below
-        // g (the base), in group order; pads past `groups` are not read as counts
+        // lane e sums expert e's counts of the raw histogram: over every group (the total)
+        // and over the groups below g (the base), in group order; pad rows past `groups` are
+        // not read
         const int sub = subs > 1 ? wv : 0;  // wave wv reads histogram wv (or the only one)
         {
             // group-major: lane e reads entry e of every group's row (each load one contiguous
