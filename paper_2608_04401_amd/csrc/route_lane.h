@@ -227,16 +227,33 @@ __device__ __forceinline__ int sorted_elbow(const float (&key)[NP], int Nn, int 
 // every kernel that selects from sorted keys alone.
 template <int NP, int KM, class OKey>
 __device__ __forceinline__ uint64_t select_first_k(const float (&key)[NP], OKey&& okey,
-                                                   int Nn, int k) {
+                                                   int Nn, int k, float* tau_out = nullptr) {
     float tau = key[0];
 #pragma unroll
     for (int i = 0; i < KM; ++i)
         if (i == k - 1) tau = key[i];
-    // common case: exactly k experts have a key >= tau (no tie at the boundary)
-    uint64_t sel = 0;
+    if (tau_out) *tau_out = tau;
+    // common case: exactly k experts have a key >= tau (no tie at the boundary).  okey(c) >= tau
+    // exactly when okey(c) - tau' is not negative, tau' being tau with a zero made -0 (so that
+    // the keys -0 and +0, equal as floats, both give +0; a finite difference keeps its sign
+    // even when it underflows): one subtraction per expert, its sign bit shifted into a word
+    // by v_alignbit, instead of a compare and a select.  tau = -inf selects every expert.
+    const float tau2 = (tau == 0.f) ? -0.f : tau;
+    constexpr int n0 = NP < 32 ? NP : 32;
+    uint32_t w0 = 0;  // after the loop, bit n0 - 1 - c: okey(c) < tau
 #pragma unroll
-    for (int c = 0; c < NP; ++c)
-        if (c < Nn && okey(c) >= tau) sel |= 1ull << c;
+    for (int c = 0; c < n0; ++c)
+        w0 = __builtin_amdgcn_alignbit(w0, __float_as_uint(okey(c) - tau2), 31);
+    uint64_t neg = __builtin_bitreverse32(w0) >> (32 - n0);
+    if constexpr (NP > 32) {
+        uint32_t w1 = 0;
+#pragma unroll
+        for (int c = 32; c < NP; ++c)
+            w1 = __builtin_amdgcn_alignbit(w1, __float_as_uint(okey(c) - tau2), 31);
+        neg |= (uint64_t)(__builtin_bitreverse32(w1) >> (64 - NP)) << 32;
+    }
+    const uint64_t real = Nn >= 64 ? ~0ull : ((1ull << Nn) - 1);
+    uint64_t sel = (tau == -INFINITY) ? real : (~neg & real);
     const bool tie = __popcll(sel) != k;
     if (__builtin_expect(__any(tie), 0)) {  // wave-uniform slow path: ties at tau
         int g = 0;  // ranks < k with a key above tau
@@ -287,7 +304,8 @@ __device__ __forceinline__ void select_emit(const float (&key)[NP], OKey&& okey,
                                             Emit&& emit) {
     constexpr int KM = NP < KMAX ? NP : KMAX;
     const float nl = neg_scaled(key[0]);
-    const uint64_t sel = select_first_k<NP, KM>(key, okey, Nn, k);
+    float tau;
+    const uint64_t sel = select_first_k<NP, KM>(key, okey, Nn, k, &tau);
     int cid[KM];
     float ck[KM];
     selected_in_id_order<NP, KM>(sel, key_of, k, cid, ck);
@@ -299,17 +317,36 @@ __device__ __forceinline__ void select_emit(const float (&key)[NP], OKey&& okey,
         denom = tree_sum<KM>(sel_u);
     }
     const float inv = 1.0f / denom;
-    // rank of each in descending order (equal keys: lower id, i.e. lower r, first)
+    // Common case, wave-uniform: the k selected keys are distinct and finite.  Then rank j's
+    // expert is the one selected expert whose key equals key[j], and its weight is u_j / S
+    // (u_j is rel_exp(key[j], nl), the same bits as from the expert's own key).
+    bool distinct = tau != -INFINITY;
 #pragma unroll
-    for (int r = 0; r < KM; ++r) {
-        if (r < k) {
-            int rank = 0;
+    for (int j = 0; j + 1 < KM; ++j)
+        if (j + 1 < k && key[j] == key[j + 1]) distinct = false;
+    if (__builtin_expect(__all(distinct), 1)) {
 #pragma unroll
-            for (int q = 0; q < KM; ++q) {
-                if (q < r) rank += (q < k && ck[q] >= ck[r]) ? 1 : 0;
-                if (q > r) rank += (q < k && ck[q] > ck[r]) ? 1 : 0;
+        for (int j = 0; j < KM; ++j) {
+            if (j < k) {
+                int id = cid[0];
+#pragma unroll
+                for (int r = 0; r < KM; ++r) id = (ck[r] == key[j]) ? cid[r] : id;
+                emit(j, id, u[j] * inv);
             }
-            emit(rank, cid[r], rel_exp(ck[r], nl) * inv);
+        }
+    } else {
+        // rank of each in descending order (equal keys: lower id, i.e. lower r, first)
+#pragma unroll
+        for (int r = 0; r < KM; ++r) {
+            if (r < k) {
+                int rank = 0;
+#pragma unroll
+                for (int q = 0; q < KM; ++q) {
+                    if (q < r) rank += (q < k && ck[q] >= ck[r]) ? 1 : 0;
+                    if (q > r) rank += (q < k && ck[q] > ck[r]) ? 1 : 0;
+                }
+                emit(rank, cid[r], rel_exp(ck[r], nl) * inv);
+            }
         }
     }
 #pragma unroll
