@@ -9,8 +9,8 @@
 //    each lane sorts its row's first half as soon as it has landed (the sorting network run
 //    in part order, sortnet.h PhasedNet) while the second is still in flight.  The tile is
 //    swizzled so that 16 lanes reading their own rows hit 16 distinct bank groups.  Each
-//    lane stages its k, ids and w in its own row of the tile and stores them itself (16-byte
-//    stores when K is the template cap).  This file is built without NaN semantics (the
+//    lane keeps its ids and w in registers and stores them itself (16-byte stores when K is
+//    the template cap).  This file is built without NaN semantics (the
 //    inputs are finite or -inf), so the raw logits are sort keys as they are.
 //  - route_kernel (any N <= 64): the rows staged through registers into a padded LDS tile;
 //    every lane routes its token from its row and stores its own outputs.
@@ -86,9 +86,7 @@ __global__ __launch_bounds__(256) void route_dma_kernel(const float* __restrict_
                                                         int* __restrict__ ids,
                                                         float* __restrict__ wout) {
     using L = DmaTile<NP>;
-    constexpr int TILE = 64 * NP;               // floats of the logit tile
-    constexpr int STG = 64 * (KMAX + 1) * 2;    // floats of the staged outputs
-    constexpr int WS = TILE > STG ? TILE : STG;
+    constexpr int WS = 64 * NP;  // floats of a wave's logit tile
     __shared__ __attribute__((aligned(1024))) float lds[4 * WS];
     const int lane = threadIdx.x & (kWave - 1);
     const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // uniform: scalar bases
@@ -135,39 +133,45 @@ __global__ __launch_bounds__(256) void route_dma_kernel(const float* __restrict_
     const int k = sorted_elbow<NP, true, KMAX>(key, NP, K, eps, mode, xt, u, S);
     if (lane < rows) kout[t0 + lane] = k;
 
-    // ---- select; each lane's outputs staged in its own row of the tile (row stride K + 1
-    // words, odd, so the 64 rows fall in distinct banks), then stored by the lane itself.
-    // Every read of the tile precedes, in program order, every write below, and a wave's LDS
-    // operations complete in order. ----
-    int* const stg_i = reinterpret_cast<int*>(tile);
-    float* const stg_w = tile + 64 * (KMAX + 1);
-    const int ld = K + 1;
+    // ---- select; each lane's outputs go to registers: the common path emits rank j with j a
+    // compile-time constant, so the unrolled select below is a plain move (the rare tie path
+    // gets a select chain), and the lane stores its own row without staging it in LDS ----
+    int oid[KMAX];
+    float ow[KMAX];
+#pragma unroll
+    for (int q = 0; q < KMAX; ++q) {
+        oid[q] = -1;
+        ow[q] = 0.f;
+    }
     select_emit<NP, true, KMAX>(
         key, [&](int c) { return okey[c]; },
         [&](int c) { return order_key(tile[L::at(lane, c)]); }, NP, K, k, u, S, renorm,
         [&](int j, int id, float w) {
-            stg_i[lane * ld + j] = id;
-            stg_w[lane * ld + j] = w;
+#pragma unroll
+            for (int q = 0; q < KMAX; ++q)
+                if (q == j) {
+                    oid[q] = id;
+                    ow[q] = w;
+                }
         });
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
     if (lane >= rows) return;
     int* const gi = ids + (t0 + lane) * K;
     float* const gw = wout + (t0 + lane) * K;
     if (vst && K == KMAX) {  // rows of KMAX values, 16-byte aligned: KMAX / 4 stores each
 #pragma unroll
         for (int q = 0; q < KMAX; q += 4) {
-            const int* si = stg_i + lane * ld + q;
-            const float* sw = stg_w + lane * ld + q;
-            *reinterpret_cast<int4*>(gi + q) = make_int4(si[0], si[1], si[2], si[3]);
-            *reinterpret_cast<float4*>(gw + q) = make_float4(sw[0], sw[1], sw[2], sw[3]);
+            *reinterpret_cast<int4*>(gi + q) =
+                make_int4(oid[q], oid[q + 1], oid[q + 2], oid[q + 3]);
+            *reinterpret_cast<float4*>(gw + q) =
+                make_float4(ow[q], ow[q + 1], ow[q + 2], ow[q + 3]);
         }
     } else {
-        for (int j = 0; j < K; ++j) {
-            gi[j] = stg_i[lane * ld + j];
-            gw[j] = stg_w[lane * ld + j];
-        }
+#pragma unroll
+        for (int q = 0; q < KMAX; ++q)
+            if (q < K) {
+                gi[q] = oid[q];
+                gw[q] = ow[q];
+            }
     }
 }
 
