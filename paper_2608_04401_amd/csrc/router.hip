@@ -327,16 +327,24 @@ __global__ __launch_bounds__(64) void route_split_sum(const float* __restrict__ 
     float u[NP], S;
     const int k = sorted_elbow<NP, true, KMAX>(key, NP, K, eps, mode, xt, u, S);
     if (valid) kout[t] = k;
-    // outputs staged in the lane's own row of tile 0 (every read of the tiles precedes, in
-    // program order, every write below; a wave's LDS operations complete in order)
-    int* const stg_i = reinterpret_cast<int*>(lds);
-    float* const stg_w = lds + 64 * (KMAX + 1);
-    const int ld = K + 1;
+    // outputs in registers (the common path emits rank j with j a compile-time constant, so
+    // the unrolled select is a plain move; the rare tie path gets a select chain)
+    int oid[KMAX];
+    float ow[KMAX];
+#pragma unroll
+    for (int q = 0; q < KMAX; ++q) {
+        oid[q] = -1;
+        ow[q] = 0.f;
+    }
     select_emit<NP, true, KMAX>(
         key, [&](int c) { return okey[c]; }, [&](int c) { return order_key(logit(c)); }, NP, K,
         k, u, S, renorm, [&](int j, int id, float w) {
-            stg_i[lane * ld + j] = id;
-            stg_w[lane * ld + j] = w;
+#pragma unroll
+            for (int q = 0; q < KMAX; ++q)
+                if (q == j) {
+                    oid[q] = id;
+                    ow[q] = w;
+                }
             if (valid && id >= 0) atomicAdd(&h[id], 1);
         });
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
@@ -344,10 +352,12 @@ __global__ __launch_bounds__(64) void route_split_sum(const float* __restrict__ 
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
     hist[lane * hist_ld + blockIdx.x] = h[lane];
     if (!valid) return;
-    for (int j = 0; j < K; ++j) {
-        ids[t * K + j] = stg_i[lane * ld + j];
-        wout[t * K + j] = stg_w[lane * ld + j];
-    }
+#pragma unroll
+    for (int q = 0; q < KMAX; ++q)
+        if (q < K) {
+            ids[t * K + q] = oid[q];
+            wout[t * K + q] = ow[q];
+        }
 }
 
 // route_split_sum_x16 (T <= 64 kDirectGroups, where one lane per token would leave most of
