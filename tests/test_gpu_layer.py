@@ -242,6 +242,17 @@ def test_forward_bf16_olmoe_prefill_all_tokens(olmoe, mode):
         print("prefill mean k %.4f" % cpu(dbg["k"]).mean())
 
 
+@pytest.mark.parametrize("T,d,N,m,K,mode", [(2048, 512, 32, 256, 4, O.MODE_ELBOW),
+                                             (1500, 384, 16, 128, 6, O.MODE_TOPK),
+                                             (3000, 256, 40, 128, 8, O.MODE_ELBOW)])
+def test_forward_bf16_other_expert_counts_all_tokens(T, d, N, m, K, mode):
+    """Whole bf16 layers with N = 32, 16 and 40 experts (the fused router with N < 64, the
+    one-lane routing at NP = 32 / 16 / 64 with pads, the dispatch with N < 64 and the grouped
+    GEMMs at other tile fills): every token against the oracle."""
+    L = synth.moe_layer(T, d, N, m, dtype="bf16", seed=T + N)
+    _forward_case(L, BF, K, mode, RTOL_BF16, label="bf16 N=%d" % N)
+
+
 def test_forward_bf16_decode_all_tokens():
     L = synth.olmoe_layer(T=64, seed=2)
     _forward_case(L, BF, 8, O.MODE_ELBOW, RTOL_BF16)
