@@ -178,7 +178,7 @@ def test_experts_bf16_olmoe_all_tokens(olmoe, mode):
 
 
 # ------------------------------------------------------------------------------ whole layer
-def _forward_case(L, dtype, K, mode, rtol, sample=None, seed=0, label="forward"):
+def _forward_case(L, dtype, K, mode, rtol, sample=None, seed=0, label="forward", renorm=False):
     """The whole layer against the oracle on every token (or a seeded sample).
 
     Routing parity is taken on the GPU's OWN fp32 logits: the oracle routes the logits the
@@ -187,17 +187,18 @@ def _forward_case(L, dtype, K, mode, rtol, sample=None, seed=0, label="forward")
     run on the GPU's routing.  The oracle's own end-to-end layer (fp64 logits) is compared
     too, on the tokens whose routing agrees with it."""
     x, Wr, Wgu, Wd = _layer_gpu(L, dtype)
-    y, dbg = B.elb_moe_forward(x, Wr, Wgu, Wd, K=K, mode=mode, debug=True)
+    y, dbg = B.elb_moe_forward(x, Wr, Wgu, Wd, K=K, mode=mode, renormalize=renorm, debug=True)
     torch.cuda.synchronize()
     tok = np.arange(L.T) if sample is None else np.sort(
         np.random.default_rng(seed).choice(L.T, sample, replace=False))
-    ref = O.moe_forward(L.x, L.W_router, L.W_gu, L.W_down, K=K, mode=mode, tokens=tok)
+    ref = O.moe_forward(L.x, L.W_router, L.W_gu, L.W_down, K=K, mode=mode, renorm=renorm,
+                        tokens=tok)
     lg = cpu(dbg["logits"])
     yy = cpu(y)
     # router logits (fp32 accumulation) against the fp64 definition
     assert rel_err_rows(lg[tok], ref.logits).max() < 1e-5
     # routing from the same fp32 logits: bit-exact outside near-ties
-    r = O.route(lg, K=K, mode=mode)
+    r = O.route(lg, K=K, mode=mode, renorm=renorm)
     near, mism = compare_routing(dbg["k"], dbg["ids"], dbg["w"], r, label)
     k, ids, w = cpu(dbg["k"]), cpu(dbg["ids"]), cpu(dbg["w"])
     same = (k == r.k) & (ids == r.ids).all(axis=1)
@@ -251,6 +252,22 @@ def test_forward_bf16_other_expert_counts_all_tokens(T, d, N, m, K, mode):
     GEMMs at other tile fills): every token against the oracle."""
     L = synth.moe_layer(T, d, N, m, dtype="bf16", seed=T + N)
     _forward_case(L, BF, K, mode, RTOL_BF16, label="bf16 N=%d" % N)
+
+
+@pytest.mark.parametrize("mode", [O.MODE_ELBOW, O.MODE_TOPK])
+def test_forward_bf16_olmoe_prefill_renormalized_all_tokens(olmoe, mode):
+    """The headline layer with renormalised weights (the selected probabilities divided by
+    their sum, as the paper's cap option allows): all 4096 tokens against the oracle."""
+    _forward_case(olmoe[0], BF, 8, mode, RTOL_BF16, label="olmoe prefill renorm", renorm=True)
+
+
+def test_forward_bf16_small_renormalized_all_tokens():
+    """Renormalised weights through the one-kernel fused router (N = 64 at T > 1024 but d not
+    a multiple of 256) and through the small-batch path (T <= 1024)."""
+    _forward_case(synth.moe_layer(1200, 320, 64, 128, dtype="bf16", seed=7), BF, 8,
+                  O.MODE_ELBOW, RTOL_BF16, label="fused renorm", renorm=True)
+    _forward_case(synth.moe_layer(300, 256, 64, 128, dtype="bf16", seed=8), BF, 8,
+                  O.MODE_ELBOW, RTOL_BF16, label="small renorm", renorm=True)
 
 
 def test_forward_bf16_decode_all_tokens():
