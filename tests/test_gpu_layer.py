@@ -270,6 +270,17 @@ def test_forward_bf16_small_renormalized_all_tokens():
                   O.MODE_ELBOW, RTOL_BF16, label="small renorm", renorm=True)
 
 
+@pytest.mark.parametrize("K", [1, 2])
+def test_forward_bf16_small_caps_all_tokens(K):
+    """Caps K = 1 (the layer is argmax routing: k = 1 for every token) and K = 2 on an
+    OLMoE-width layer at T = 2048 (the split router; few rows per expert, so the 128-row GEMM
+    tiles): every token against the oracle."""
+    L = synth.moe_layer(2048, 2048, 64, 256, dtype="bf16", seed=30 + K)
+    y, dbg = _forward_case(L, BF, K, O.MODE_ELBOW, RTOL_BF16, label="K=%d" % K)
+    if K == 1:
+        assert (cpu(dbg["k"]) == 1).all()
+
+
 def test_forward_bf16_decode_all_tokens():
     L = synth.olmoe_layer(T=64, seed=2)
     _forward_case(L, BF, 8, O.MODE_ELBOW, RTOL_BF16)
