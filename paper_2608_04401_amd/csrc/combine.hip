@@ -7,13 +7,16 @@
 // expert row is read with 16-byte coalesced loads.  The token's slots are taken eight at a
 // time: their rows and weights first, then all eight row loads at once, then the FMAs in rank
 // order, so a block waits for memory once per eight experts instead of twice per expert.
-// (Plain loads: Y was just written by the down GEMM, and non-temporal loads measured slower.)
 #include "common.h"
 
 namespace elb {
 
 namespace {
 
+// NT: the rows are loaded with the non-temporal hint (chosen when Y is larger than the
+// last-level cache, so that it streams from HBM; a smaller Y that the down GEMM has just
+// written is read faster with plain loads)
+template <bool NT>
 __global__ __launch_bounds__(256) void combine_bf16(const bf16_t* __restrict__ Y,
                                                     const int* __restrict__ k,
                                                     const int* __restrict__ inv,
@@ -46,11 +49,14 @@ __global__ __launch_bounds__(256) void combine_bf16(const bf16_t* __restrict__ Y
                     wj[q] = w[t * K + j];
                 }
             }
-            uint4 yq[8];
+            u32x4_t yq[8];
 #pragma unroll
-            for (int q = 0; q < 8; ++q)
-                yq[q] = r[q] >= 0 ? *reinterpret_cast<const uint4*>(Y + r[q] * d + c)
-                                  : make_uint4(0u, 0u, 0u, 0u);
+            for (int q = 0; q < 8; ++q) {
+                const u32x4_t* const src = reinterpret_cast<const u32x4_t*>(Y + r[q] * d + c);
+                yq[q] = r[q] < 0 ? u32x4_t{0u, 0u, 0u, 0u}
+                        : NT     ? __builtin_nontemporal_load(src)
+                                 : *src;
+            }
 #pragma unroll
             for (int q = 0; q < 8; ++q) {
                 if (r[q] < 0) continue;  // slots past k_t, and dropped ones, add nothing
@@ -117,8 +123,15 @@ hipError_t launch_combine(const void* Y, const int* k, const int* inv, const flo
     if (T == 0) return hipSuccess;
     if (dtype == ELB_BF16) {
         ProfileScope prof("combine_bf16", s);
-        ELB_LAUNCH(combine_bf16, dim3((unsigned)T), dim3(256), 0, s, (const bf16_t*)Y, k,
-                           inv, w, (const bf16_t*)residual, T, d, K, (bf16_t*)y);
+        // Y holds at most T K rows of d bf16 values
+        const bool nt = (double)T * K * d * 2 > (double)kLastLevelCacheBytes;
+        if (nt)
+            ELB_LAUNCH(combine_bf16<true>, dim3((unsigned)T), dim3(256), 0, s, (const bf16_t*)Y,
+                       k, inv, w, (const bf16_t*)residual, T, d, K, (bf16_t*)y);
+        else
+            ELB_LAUNCH(combine_bf16<false>, dim3((unsigned)T), dim3(256), 0, s,
+                       (const bf16_t*)Y, k, inv, w, (const bf16_t*)residual, T, d, K,
+                       (bf16_t*)y);
     } else {
         ProfileScope prof("combine_f32", s);
         ELB_LAUNCH(combine_f32, dim3((unsigned)T), dim3(256), 0, s, (const float*)Y, k,

@@ -140,6 +140,9 @@ hipError_t launch_gemm_skinny(const void* x, const void* Wgu, const void* Wd, co
 hipError_t launch_pack_experts(const void* Wgu, const void* Wd, int N, int d, int m,
                                void* packed, hipStream_t s);
 
+// MI355X's last-level (Infinity) cache: data larger than this streams from HBM
+constexpr size_t kLastLevelCacheBytes = (size_t)256 << 20;
+
 // combine: y[t] = residual[t] + sum_j w[t, j] Y[inv[t, j]]  (inv == nullptr: row t K + j)
 hipError_t launch_combine(const void* Y, const int* k, const int* inv, const float* w,
                           const void* residual, int64_t T, int d, int K, int dtype, void* y,
