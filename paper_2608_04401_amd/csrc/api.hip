@@ -475,9 +475,10 @@ static int moe_forward_entry(const void* x, const void* W_router, const void* W_
     float* w = w_out ? w_out : (float*)(ws + L.w);
     // Router and routing, by size (the same bits on every path): large batches with N = 64
     // and d % 256 == 0 split the contraction over four blocks per 64 tokens (two launches; the
-    // second also writes the dispatch histogram); small batches with N = 64 use the
-    // expert-split router and the 16-lane routing; the rest the fused one-block kernel, or the
-    // router and routing kernels for fp32 and caps above 16.
+    // second also writes the dispatch histogram); small batches with N = 64 take one wave per
+    // (16 tokens, 16 experts, quarter of the contraction), then the same 16-lane split
+    // routing; the rest the fused one-block kernel, or the router and routing kernels for
+    // fp32 and caps above 16.
     const bool skinny = gemm_use_skinny(dtype, T, K, N, d, m);
     if (router_split_usable(dtype, T, d, N, K) && !skinny) {
         if (int rc = hip_status(
@@ -485,6 +486,16 @@ static int moe_forward_entry(const void* x, const void* W_router, const void* W_
                                           logits_out, k, ids, w, (int*)(ws + L.hist),
                                           dispatch_hist_ld(T), s),
                 "router_split_route"))
+            return rc;
+        return experts_impl(x, W_gate_up, W_down, packed, k, ids, w, residual, T, d, N, m, K,
+                            dtype, y, ws, L, counts_out, s, true, split_hist_subs(T));
+    }
+    if (router_slices_usable(dtype, T, N, K)) {
+        if (int rc = hip_status(
+                launch_router_slices_route(x, W_router, T, d, *params, (float*)(ws + L.part),
+                                           logits_out, k, ids, w, (int*)(ws + L.hist),
+                                           dispatch_hist_ld(T), s),
+                "router_slices_route"))
             return rc;
         return experts_impl(x, W_gate_up, W_down, packed, k, ids, w, residual, T, d, N, m, K,
                             dtype, y, ws, L, counts_out, s, true, split_hist_subs(T));

@@ -114,6 +114,16 @@ hipError_t launch_router_split_route(const void* x, const void* Wr, int64_t T, i
                                      int* k, int* ids, float* w, int* hist, int64_t hist_ld,
                                      hipStream_t s);
 
+// the layer's router and routing for batches of at most kSmallBatch tokens with N == 64
+// (bf16, K <= kLaneMaxK): one wave per (16 tokens, 16 experts, quarter of the contraction)
+// into part [4, T, 64], then the 16-lane split routing (histograms as above, split_hist_subs(T)
+// of them).  Same bits as the other router paths.
+bool router_slices_usable(int dtype, int64_t T, int N, int K);
+hipError_t launch_router_slices_route(const void* x, const void* Wr, int64_t T, int d,
+                                      const elb_route_params& p, float* part, float* logits,
+                                      int* k, int* ids, float* w, int* hist, int64_t hist_ld,
+                                      hipStream_t s);
+
 // grouped GEMMs
 // rows per M-tile of the grouped GEMMs for this problem (the dispatch scan uses the same)
 int gemm_tile_rows(int dtype, int64_t T, int K, int N, int d, int m);

@@ -30,13 +30,14 @@ __device__ __forceinline__ void router_slice(int d, int s, int& first, int& coun
 // each wave's partial sums over its k-steps go to part[w] (lane rows, expert columns
 // 16 g + ..., g < NG); the caller sums the RW partial tiles.  Every logit is computed the same
 // way whatever NG and g0 are (its own MFMA column, the same k-steps per wave, the same sum).
+// w: the slice (by default the wave's index in the block).
 template <int NG>
 __device__ __forceinline__ void router_partials(const bf16_t* __restrict__ x,
                                                 const bf16_t* __restrict__ Wr, int64_t T,
                                                 int d, int N, int64_t t0, int g0,
-                                                float (&part)[RW][16][65]) {
+                                                float (&part)[RW][16][65],
+                                                int w = threadIdx.x >> 6) {
     const int lane = threadIdx.x & 63;
-    const int w = threadIdx.x >> 6;
     const int l16 = lane & 15;
     const int kq = (lane >> 4) * 8;
     const int64_t ta = t0 + l16;
@@ -125,6 +126,31 @@ __global__ __launch_bounds__(64 * RW) void router_bf16(const bf16_t* __restrict_
         const int64_t t = t0 + tr;
         const int n = 16 * g0 + nl;
         if (t < T && n < N) logits[t * N + n] = router_sum(part, tr, nl);
+    }
+}
+
+// Batches of at most kSmallBatch tokens with N = 64 (decode): one wave per (16 tokens, 16
+// experts, slice s of the contraction), so that the x and W_r reads spread over four times as
+// many compute units as in router_bf16<1> (32 KB per block instead of 128 KB); the partial
+// tile goes to part [4, T, 64], and route_split_sum_x16 sums the four slices in order and
+// routes them (the same bits as router_bf16's LDS sum and every other router path).
+__global__ __launch_bounds__(64) void router_slice_bf16(const bf16_t* __restrict__ x,
+                                                        const bf16_t* __restrict__ Wr,
+                                                        int64_t T, int d,
+                                                        float* __restrict__ part) {
+    __shared__ float tile[RW][16][65];  // only row blockIdx.z is used
+    const int64_t t0 = (int64_t)blockIdx.x * 16;
+    const int g0 = (int)blockIdx.y, s = (int)blockIdx.z;
+    router_partials<1>(x, Wr, T, d, 64, t0, g0, tile, s);
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        const int o = threadIdx.x + 64 * q;
+        const int tr = o >> 4, nl = o & 15;
+        const int64_t t = t0 + tr;
+        if (t < T) part[((int64_t)s * T + t) * 64 + 16 * g0 + nl] = tile[s][tr][nl];
     }
 }
 
@@ -503,6 +529,32 @@ hipError_t launch_router_split_route(const void* x, const void* Wr, int64_t T, i
     else
         ELB_LAUNCH(route_split_sum<kLaneMaxK>, dim3(groups), dim3(64), 0, s, part, T, p.K,
                    p.eps, p.mode, p.renormalize, xt, logits, k, ids, w, hist, hist_ld);
+    return hipGetLastError();
+}
+
+bool router_slices_usable(int dtype, int64_t T, int N, int K) {
+    return dtype == ELB_BF16 && N == 64 && K <= kLaneMaxK && T > 0 && T <= kSmallBatch;
+}
+
+hipError_t launch_router_slices_route(const void* x, const void* Wr, int64_t T, int d,
+                                      const elb_route_params& p, float* part, float* logits,
+                                      int* k, int* ids, float* w, int* hist, int64_t hist_ld,
+                                      hipStream_t s) {
+    if (T == 0) return hipSuccess;
+    {
+        ProfileScope prof("router_bf16", s);
+        ELB_LAUNCH(router_slice_bf16, dim3((unsigned)((T + 15) / 16), 4, RW), dim3(64), 0, s,
+                   (const bf16_t*)x, (const bf16_t*)Wr, T, d, part);
+    }
+    ProfileScope prof("route", s);
+    const dim3 grid((unsigned)(dispatch_groups(T) * kHistSubs));
+    const XTable xt = make_xtable(64);
+    if (p.K <= 8)
+        ELB_LAUNCH(route_split_sum_x16<8>, grid, dim3(256), 0, s, part, T, p.K, p.eps, p.mode,
+                   p.renormalize, xt, logits, k, ids, w, hist, hist_ld);
+    else
+        ELB_LAUNCH(route_split_sum_x16<kLaneMaxK>, grid, dim3(256), 0, s, part, T, p.K, p.eps,
+                   p.mode, p.renormalize, xt, logits, k, ids, w, hist, hist_ld);
     return hipGetLastError();
 }
 

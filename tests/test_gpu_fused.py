@@ -88,3 +88,25 @@ def test_layer_split_router_equals_fused(T, d, K, mode):
                         cpu(w)[tok].astype(np.float64), tokens=tok)
     rel = rel_err_rows(cpu(y)[tok], ref)
     assert rel.max() < RTOL_BF16, rel.max()
+
+
+@pytest.mark.parametrize("T,d,K,mode", [(64, 2048, 8, B.MODE_ELBOW), (5, 512, 8, B.MODE_TOPK),
+                                        (1024, 256, 16, B.MODE_ELBOW), (333, 768, 12, B.MODE_ELBOW)])
+def test_layer_small_batch_router_equals_fused(T, d, K, mode):
+    """Batches of at most 1024 tokens with N = 64: the layer computes the router as one wave
+    per (16 tokens, 16 experts, quarter of the contraction) and sums the quarters in the
+    16-lane split routing.  Its logits, k, ids and w must be the one-block fused kernel's bits,
+    its per-expert counts those of its routing, and its output the expert stage's bits on the
+    same routing."""
+    L = synth.moe_layer(T, d, 64, 128, dtype="bf16", seed=T + d + 1)
+    x, Wr, Wgu, Wd = (to_gpu(a, BF) for a in (L.x, L.W_router, L.W_gu, L.W_down))
+    y, dbg = B.elb_moe_forward(x, Wr, Wgu, Wd, K=K, mode=mode, debug=True)
+    k, ids, w, lg = B.elb_router_route(x, Wr, K=K, mode=mode, with_logits=True)
+    torch.cuda.synchronize()
+    assert torch.equal(dbg["logits"], lg)
+    assert torch.equal(dbg["k"], k) and torch.equal(dbg["ids"], ids) and torch.equal(dbg["w"], w)
+    kk, ii = cpu(k), cpu(ids)
+    assert np.array_equal(cpu(dbg["counts"]), np.bincount(ii[ii >= 0], minlength=64))
+    y2 = B.elb_moe_experts(x, Wgu, Wd, k, ids, w)
+    torch.cuda.synchronize()
+    assert torch.equal(y, y2)
