@@ -280,14 +280,20 @@ __global__ __launch_bounds__(64 * kScatterWaves) void dispatch_scatter(
     const uint64_t below = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
     const int per = (N + kScatterWaves - 1) / kScatterWaves;
     const int e0 = wv * per, e1 = e0 + per < N ? e0 + per : N;
-    for (int e = e0; e < e1; ++e) {
-        const bool has = (mask >> e) & 1ull;
-        const uint64_t b = __ballot(has);
-        const int base = __builtin_amdgcn_readlane(base_mine, e);  // e is wave-uniform
-        if (has) {
-            const int r = base + __popcll(b & below);
-            row_token[r] = (int)t;
-            pos[lane][e] = r;
+    // a fixed trip count (N <= 64), unrolled, so that the experts' ballots and lane reads
+    // overlap instead of forming one dependent chain
+#pragma unroll
+    for (int i = 0; i < kWave / kScatterWaves; ++i) {
+        const int e = e0 + i;
+        if (e < e1) {  // wave-uniform
+            const bool has = (mask >> e) & 1ull;
+            const uint64_t b = __ballot(has);
+            const int base = __builtin_amdgcn_readlane(base_mine, e);
+            if (has) {
+                const int r = base + __popcll(b & below);
+                row_token[r] = (int)t;
+                pos[lane][e] = r;
+            }
         }
     }
     __syncthreads();
