@@ -542,11 +542,11 @@ hipError_t launch_router_slices_route(const void* x, const void* Wr, int64_t T, 
                                       hipStream_t s) {
     if (T == 0) return hipSuccess;
     {
-        ProfileScope prof("router_bf16", s);
+        ProfileScope prof("router_slice_bf16", s);
         ELB_LAUNCH(router_slice_bf16, dim3((unsigned)((T + 15) / 16), 4, RW), dim3(64), 0, s,
                    (const bf16_t*)x, (const bf16_t*)Wr, T, d, part);
     }
-    ProfileScope prof("route", s);
+    ProfileScope prof("route_split_sum", s);
     const dim3 grid((unsigned)(dispatch_groups(T) * kHistSubs));
     const XTable xt = make_xtable(64);
     if (p.K <= 8)
