@@ -250,7 +250,8 @@ int elb_router_logits(const void* x, const void* W_router, int64_t T, int32_t d,
     if (int rc = check_dtype(dtype)) return rc;
     if (T < 0) return fail(ELB_ERR_INVALID_ARG, "T = %lld < 0", (long long)T);
     if (N < 2) return fail(ELB_ERR_INVALID_ARG, "N = %d: need at least 2 experts", N);
-    if (N > ELB_MAX_EXPERTS) return fail(ELB_ERR_UNSUPPORTED, "N = %d exceeds %d", N, ELB_MAX_EXPERTS);
+    if (N > ELB_MAX_EXPERTS)
+        return fail(ELB_ERR_UNSUPPORTED, "N = %d exceeds %d", N, ELB_MAX_EXPERTS);
     if (d < 1) return fail(ELB_ERR_INVALID_ARG, "d = %d < 1", d);
     if (dtype == ELB_BF16 && d % 32)
         return fail(ELB_ERR_INVALID_ARG, "bf16 router needs d %% 32 == 0 (d = %d)", d);
@@ -331,7 +332,8 @@ int elb_dispatch(const int32_t* k, const int32_t* ids, int64_t T, int32_t N, int
     g_err.clear();
     if (T < 0) return fail(ELB_ERR_INVALID_ARG, "T = %lld < 0", (long long)T);
     if (N < 2) return fail(ELB_ERR_INVALID_ARG, "N = %d: need at least 2 experts", N);
-    if (N > ELB_MAX_EXPERTS) return fail(ELB_ERR_UNSUPPORTED, "N = %d exceeds %d", N, ELB_MAX_EXPERTS);
+    if (N > ELB_MAX_EXPERTS)
+        return fail(ELB_ERR_UNSUPPORTED, "N = %d exceeds %d", N, ELB_MAX_EXPERTS);
     if (K < 1 || K > N) return fail(ELB_ERR_INVALID_ARG, "K = %d outside [1, N = %d]", K, N);
     if (T * (int64_t)K >= (int64_t)1 << 31)
         return fail(ELB_ERR_UNSUPPORTED, "T * K exceeds 2^31");
@@ -412,10 +414,10 @@ static int experts_impl(const void* x, const void* W_gate_up, const void* W_down
 }
 
 static int moe_experts_entry(const void* x, const void* W_gate_up, const void* W_down,
-                             const void* packed,
-                    const int32_t* k, const int32_t* ids, const float* w, const void* residual,
-                    int64_t T, int32_t d, int32_t N, int32_t m, int32_t K, int32_t dtype,
-                    void* y, void* workspace, size_t workspace_bytes, void* stream) {
+                             const void* packed, const int32_t* k, const int32_t* ids,
+                             const float* w, const void* residual, int64_t T, int32_t d,
+                             int32_t N, int32_t m, int32_t K, int32_t dtype, void* y,
+                             void* workspace, size_t workspace_bytes, void* stream) {
     g_err.clear();
     if (int rc = check_expert_dims(T, d, N, m, K, dtype)) return rc;
     if (T == 0) return ELB_OK;
@@ -427,8 +429,8 @@ static int moe_experts_entry(const void* x, const void* W_gate_up, const void* W
                     L.experts_end);
     if ((uintptr_t)workspace % kAlign)
         return fail(ELB_ERR_WORKSPACE, "workspace not %zu-byte aligned", kAlign);
-    return experts_impl(x, W_gate_up, W_down, packed, k, ids, w, residual, T, d, N, m, K, dtype, y,
-                        (char*)workspace, L, nullptr, (hipStream_t)stream);
+    return experts_impl(x, W_gate_up, W_down, packed, k, ids, w, residual, T, d, N, m, K,
+                        dtype, y, (char*)workspace, L, nullptr, (hipStream_t)stream);
 }
 
 int elb_moe_experts(const void* x, const void* W_gate_up, const void* W_down,
@@ -449,11 +451,12 @@ int elb_moe_experts_packed(const void* x, const void* W_gate_up, const void* W_d
 }
 
 static int moe_forward_entry(const void* x, const void* W_router, const void* W_gate_up,
-                             const void* W_down, const void* packed, const void* residual, int64_t T, int32_t d, int32_t N,
-                    int32_t m, int32_t dtype, const elb_route_params* params, void* y,
-                    void* workspace, size_t workspace_bytes, float* logits_out,
-                    int32_t* k_out, int32_t* ids_out, float* w_out, int32_t* counts_out,
-                    void* stream) {
+                             const void* W_down, const void* packed, const void* residual,
+                             int64_t T, int32_t d, int32_t N, int32_t m, int32_t dtype,
+                             const elb_route_params* params, void* y, void* workspace,
+                             size_t workspace_bytes, float* logits_out, int32_t* k_out,
+                             int32_t* ids_out, float* w_out, int32_t* counts_out,
+                             void* stream) {
     g_err.clear();
     if (int rc = check_route_params(N, params)) return rc;
     if (int rc = check_expert_dims(T, d, N, m, params->K, dtype)) return rc;
@@ -511,8 +514,8 @@ static int moe_forward_entry(const void* x, const void* W_router, const void* W_
         if (int rc = hip_status(launch_route(logits, T, N, *params, k, ids, w, s), "route"))
             return rc;
     }
-    return experts_impl(x, W_gate_up, W_down, packed, k, ids, w, residual, T, d, N, m, K, dtype, y, ws,
-                        L, counts_out, s);
+    return experts_impl(x, W_gate_up, W_down, packed, k, ids, w, residual, T, d, N, m, K,
+                        dtype, y, ws, L, counts_out, s);
 }
 
 int elb_moe_forward(const void* x, const void* W_router, const void* W_gate_up,

@@ -107,7 +107,8 @@ __global__ __launch_bounds__(256) void route_dma_kernel(const float* __restrict_
             const int cc = (local % L::CP) ^ L::swz(r);
             const int rs = r < rows ? r : rows - 1;  // rows past T: a valid row, never used
             const uint32_t va = (uint32_t)(rs * NP + (p * L::CP + cc) * 4) * 4u;
-            const uint32_t la = __builtin_amdgcn_readfirstlane(lds0 + (p * 64 * L::CP + j * 64) * 16);
+            const uint32_t la =
+                __builtin_amdgcn_readfirstlane(lds0 + (p * 64 * L::CP + j * 64) * 16);
             // non-temporal: the logits are read once (measured: -3 % at T = 65536 and 2^20)
             asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2 nt"
                          :: "s"(la), "v"(va), "s"(src) : "memory", "m0");

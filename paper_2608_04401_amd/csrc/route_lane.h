@@ -412,7 +412,9 @@ __device__ __forceinline__ int xor16(int v) {
     }
 }
 template <int M>
-__device__ __forceinline__ float xor16f(float v) { return __int_as_float(xor16<M>(__float_as_int(v))); }
+__device__ __forceinline__ float xor16f(float v) {
+    return __int_as_float(xor16<M>(__float_as_int(v)));
+}
 template <int M>
 __device__ __forceinline__ int64_t xor16_64(int64_t v) {
     const int lo = xor16<M>((int)(uint32_t)v);

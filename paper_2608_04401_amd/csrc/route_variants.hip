@@ -7,8 +7,8 @@
 // sorting network carries the expert ids along with the logits, so the id at every rank is
 // known and any cap up to N costs the same.  Same bits as the routing kernel: the same keys,
 // u_i = exp(l_(i) - l_(0)) in rank order (rel_exp), S as the same tree over the ranks
-// (tree_sum), the same E_i and first argmin, w = u * (1 / denominator).  The elbow angle (no selection asked for) and
-// tail randomisation with K <= 16 sort the keys only.
+// (tree_sum), the same E_i and first argmin, w = u * (1 / denominator).  The elbow angle (no
+// selection asked for) and tail randomisation with K <= 16 sort the keys only.
 #include "route_lane.h"
 
 namespace elb {
@@ -332,10 +332,14 @@ hipError_t launch_route_pair(const float* logits, const float* rand, int64_t T, 
         case 32: launch_pair_np<32, true>(logits, rand, T, N, p, k, ids, w, e, theta, s); break;
         case 64: launch_pair_np<64, true>(logits, rand, T, N, p, k, ids, w, e, theta, s); break;
         default:
-            if (N < 8) launch_pair_np<8, false>(logits, rand, T, N, p, k, ids, w, e, theta, s);
-            else if (N < 16) launch_pair_np<16, false>(logits, rand, T, N, p, k, ids, w, e, theta, s);
-            else if (N < 32) launch_pair_np<32, false>(logits, rand, T, N, p, k, ids, w, e, theta, s);
-            else launch_pair_np<64, false>(logits, rand, T, N, p, k, ids, w, e, theta, s);
+            if (N < 8)
+                launch_pair_np<8, false>(logits, rand, T, N, p, k, ids, w, e, theta, s);
+            else if (N < 16)
+                launch_pair_np<16, false>(logits, rand, T, N, p, k, ids, w, e, theta, s);
+            else if (N < 32)
+                launch_pair_np<32, false>(logits, rand, T, N, p, k, ids, w, e, theta, s);
+            else
+                launch_pair_np<64, false>(logits, rand, T, N, p, k, ids, w, e, theta, s);
     }
     return hipGetLastError();
 }
