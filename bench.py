@@ -89,6 +89,29 @@ def settle(B, torch, args_gpu, K, seconds):
     return n
 
 
+def graph_replay(B, torch, args_gpu, K, mode, steps):
+    """ms per layer call with one call captured in a HIP graph (torch.cuda.CUDAGraph around
+    the C-ABI call) and the graph replayed `steps` times: the same kernels without the host
+    work of a call or launch gaps between them."""
+    x, Wr, Wgu, Wd = args_gpu
+    out = torch.empty_like(x)
+    B.elb_moe_forward(x, Wr, Wgu, Wd, K=K, mode=mode, out=out)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        B.elb_moe_forward(x, Wr, Wgu, Wd, K=K, mode=mode, out=out)
+    for _ in range(3):
+        g.replay()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(steps):
+        g.replay()
+    e1.record()
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / steps
+
+
 def headline(B, torch, args_gpu, K, steps, warmup, blocks=5):
     """The headline timing: exactly `steps` elbow-routed layer calls, split into blocks that
     alternate with blocks of the fixed top-K routing on the same inputs (which block of a pair
@@ -713,6 +736,9 @@ def main():
     # kernels from the loops that time every launch (a few us high each)
     kern = {n: kern_g.get(n, v) for n, v in kern.items()}
     kern_top = {n: kern_gt.get(n, v) for n, v in kern_top.items()}
+    # the same layer call captured in a HIP graph and replayed (launch gaps and host work gone)
+    ms_graph = {name: graph_replay(B, torch, gpu, K, mode, args.steps)
+                for name, mode in (("elbow", B.MODE_ELBOW), ("topk", B.MODE_TOPK))}
 
     # the grouped GEMMs' kernels (the small-tile variants carry a "_s" suffix)
     g1 = next(n for n in kern if n.startswith("gemm_gate_up"))
@@ -774,6 +800,7 @@ def main():
                          "other kernels from a loop timing every launch, which runs each "
                          "kernel a few us slow",
         "ms_per_step_gemm_timing_loop": round(ms_ev_g, 4),
+        "ms_per_step_graph_replay": {n: round(v, 4) for n, v in ms_graph.items()},
         "kernel_sum_ms": round(kern_sum, 4),
         "ms_per_step_with_kernel_events": round(ms_ev, 4),
         "topk_baseline": {
