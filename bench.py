@@ -651,6 +651,37 @@ def calibration(B, torch):
     return out
 
 
+def token_sweep(B, torch, synth, Ts, K=8, steps=20):
+    """The OLMoE-shaped layer (stack layer 0's weights, drawn on the device) at several batch
+    sizes T: ms per call for elbow and top-K routing in alternating blocks after 0.3 s of
+    untimed calls, the expert GEMMs' times and the gate/up GEMM's fraction of the bf16 MFMA
+    peak.  The library picks each size's kernels (row-major weights)."""
+    Wr, Wgu, Wd = synth.device_stack_layer(0)
+    d, m = Wr.shape[1], Wd.shape[2]
+    rows = []
+    for T in Ts:
+        x = synth.device_stack_input(T, d)
+        gpu = (x, Wr, Wgu, Wd)
+        _, dbg = B.elb_moe_forward(x, Wr, Wgu, Wd, K=K, debug=True)
+        sum_k = int(dbg["k"].sum().item())
+        settle(B, torch, gpu, K, 0.3)
+        hl = headline(B, torch, gpu, K, steps, 2)
+        _, kern = time_layer(B, torch, gpu, K, B.MODE_ELBOW, steps, 2, 2)
+        g1 = next(n for n in kern if n.startswith("gemm_gate_up"))
+        g2 = next(n for n in kern if n.startswith("gemm_down"))
+        ms = hl["elbow"]["ms_per_step"]
+        rows.append({"T": T, "mean_k": round(sum_k / T, 4),
+                     "elbow_ms": round(ms, 4), "topk_ms": round(hl["topk"]["ms_per_step"], 4),
+                     "tokens_per_s": round(T / (ms * 1e-3), 1),
+                     "gate_up_kernel": g1, "gate_up_us": round(kern[g1] * 1e3, 2),
+                     "down_us": round(kern[g2] * 1e3, 2),
+                     "gate_up_frac_of_bf16_peak": round(
+                         4.0 * d * m * sum_k / (kern[g1] * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4)})
+        log("sweep T=%d: %.4f ms elbow, %.4f ms top-K" % (T, ms, hl["topk"]["ms_per_step"]))
+        del x, gpu, dbg
+    return rows
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -671,6 +702,9 @@ def main():
     ap.add_argument("--routing-counters", action="store_true",
                     help="run only the routing kernel on the routing-only workload (for "
                          "instruction counter runs)")
+    ap.add_argument("--sweep-tokens", default="",
+                    help="comma-separated batch sizes: print only the OLMoE-shaped layer's "
+                         "timing at each (one JSON line)")
     ap.add_argument("--traffic-from", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
                     help="write the gate/up GEMM traffic file from two rocprofv3 counter CSVs")
     ap.add_argument("--traffic-command", default="",
@@ -694,6 +728,10 @@ def main():
     B.lib()
     if args.routing_counters:
         routing_only(B, torch, nbuf=4, iters=args.steps)
+        return
+    if args.sweep_tokens:
+        Ts = [int(v) for v in args.sweep_tokens.split(",") if v]
+        print(json.dumps({"token_sweep": token_sweep(B, torch, synth, Ts, steps=args.steps)}))
         return
     T, d, N, m, K = WORKLOADS[args.workload]
     log("generating %s inputs T=%d d=%d N=%d m=%d" % (args.workload, T, d, N, m))

@@ -228,6 +228,17 @@ def _forward_case(L, dtype, K, mode, rtol, sample=None, seed=0, label="forward",
     return y, dbg
 
 
+@pytest.mark.parametrize("T", [768, 1024])
+@pytest.mark.parametrize("mode", [O.MODE_ELBOW, O.MODE_TOPK])
+def test_forward_bf16_olmoe_mid_batches_all_tokens(olmoe, T, mode):
+    """The headline layer's weights at mid-sized batches (the first T of its tokens): 90 to
+    128 rows per expert, where the 256-row tile kernel takes over from the 128-row one (most
+    experts fill less than half of their one M-tile), on every token."""
+    L = olmoe[0]
+    Lt = synth.LayerInputs(L.x[:T].copy(), L.W_router, L.W_gu, L.W_down, L.dtype)
+    _forward_case(Lt, BF, 8, mode, RTOL_BF16, label="olmoe T=%d" % T)
+
+
 def test_forward_f32_tiny_all_tokens():
     _forward_case(synth.tiny_layer(seed=0), torch.float32, 8, O.MODE_ELBOW, RTOL_F32)
     _forward_case(synth.tiny_layer(seed=1), torch.float32, 2, O.MODE_ELBOW, RTOL_F32)
