@@ -399,14 +399,15 @@ static int experts_impl(const void* x, const void* W_gate_up, const void* W_down
                             "dispatch"))
         return rc;
     {
+        const bool ntw = gemm_stream_weights(T, K, N);
         if (int rc = hip_status(launch_gemm_gate_up(x, W_gate_up, row_token, offsets, tile_off,
                                                     big ? tail_list : nullptr, mt, tr, d, N, m,
-                                                    dtype, H, s),
+                                                    dtype, H, s, ntw),
                                 "gemm_gate_up"))
             return rc;
         if (int rc = hip_status(launch_gemm_down(H, W_down, offsets, tile_off,
                                                  big ? tail_list : nullptr, mt, tr, d, N, m,
-                                                 dtype, Y, s),
+                                                 dtype, Y, s, ntw),
                                 "gemm_down"))
             return rc;
     }

@@ -128,15 +128,22 @@ hipError_t launch_router_slices_route(const void* x, const void* Wr, int64_t T, 
 // rows per M-tile of the grouped GEMMs for this problem (the dispatch scan uses the same)
 int gemm_tile_rows(int dtype, int64_t T, int K, int N, int d, int m);
 // tail_list (large-tile kernels only, TilePlan): its experts' remainder rows are computed
-// by extra blocks of the same launch
+// by extra blocks of the same launch.  nt_weights (large-tile kernels): the weight copies carry
+// the non-temporal hint (gemm_stream_weights)
 hipError_t launch_gemm_gate_up(const void* x, const void* Wgu, const int* row_token,
                                const int* offsets, const int* tile_off, const int* tail_list,
                                int64_t max_tiles, int tile_rows, int d, int N, int m,
-                               int dtype, void* H, hipStream_t s);
+                               int dtype, void* H, hipStream_t s, bool nt_weights);
 hipError_t launch_gemm_down(const void* H, const void* Wd, const int* offsets,
                             const int* tile_off, const int* tail_list, int64_t max_tiles,
                             int tile_rows, int d, int N, int m, int dtype, void* Y,
-                            hipStream_t s);
+                            hipStream_t s, bool nt_weights);
+// whether the large-tile GEMMs stream the weights with the non-temporal hint: yes while an
+// expert has at most about three M-tiles of rows (its weight tiles are read by few blocks),
+// no above, where the tiles are read by many blocks and are better kept in the caches
+inline bool gemm_stream_weights(int64_t T, int K, int N) {
+    return T * K < (int64_t)768 * (N > 0 ? N : 1);
+}
 
 // decode-sized batches: weight-streaming gate/up (+SwiGLU) and down GEMMs, both launched
 bool gemm_use_skinny(int dtype, int64_t T, int K, int N, int d, int m);

@@ -224,12 +224,13 @@ __global__ __launch_bounds__(256) void gemm_bf16(const bf16_t* __restrict__ A,
 // 128 x 128, v_mfma_f32_32x32x16_bf16, one block per CU (the copy ring takes all 160 KB of LDS).
 //
 // Copies: global_load_lds_dwordx4 (no staging registers, no ds_write).  Each copy
-// instruction moves 8 rows x 128 bytes, one whole cache line per row: the copy rate is bound
-// by the misses a CU's vector cache can keep in flight, so full lines move twice the bytes
-// per miss of half lines.  Weight copies carry the non-temporal hint: each weight tile is
-// read by the one or two M-tiles of its expert, close together in time, and streaming it
-// keeps the caches for the token rows and for the other GEMM's operands (measured: down
-// GEMM -8 %, gate/up unchanged).  The A half (token rows) and the B half (weight rows) of a k-tile
+// instruction moves 8 rows x 128 bytes, one whole cache line per row (full lines move more
+// bytes per request than half lines).  With up to three M-tiles per expert the weight copies
+// carry the non-temporal hint: each weight tile is read by the few M-tiles of its expert,
+// close together in time, and streaming it keeps the caches for the token rows and for the
+// other GEMM's operands (measured: down GEMM -8 %, gate/up unchanged); with more M-tiles the
+// tiles are reused enough that the hint costs more than it saves, so the kernel takes it as an
+// argument.  The A half (token rows) and the B half (weight rows) of a k-tile
 // are separate 32 KB units of a 5-unit ring; the B half, which usually misses to HBM, is
 // issued two k-tiles ahead of its use and the A half one k-tile ahead.  LDS rows are
 // unpadded (128 B) with their eight 16-byte chunks XOR-swizzled per row so that the 16
@@ -324,21 +325,19 @@ __device__ __forceinline__ void tail_block(const bf16_t* __restrict__ A,
     else tail_task<MODE, 2>(wp, xp, s0, s1, rows, row0, out_ld, out_col, C, lds);
 }
 
-template <int MODE>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) void gemm_bf16_dma(
+// NTW: the weight copies carry the non-temporal hint (the kernel below picks it by size)
+template <int MODE, bool NTW>
+__device__ __forceinline__ void gemm_dma_body(
     const bf16_t* __restrict__ A, const int* __restrict__ row_token,
     const bf16_t* __restrict__ B, const int* __restrict__ offsets,
     const int* __restrict__ tile_off, const int* __restrict__ tail_list, int big_blocks,
-    int N, int d, int m, bf16_t* __restrict__ C) {
+    int N, int d, int m, bf16_t* __restrict__ C, char* sm_bytes) {
     constexpr int TM = 256, TN = 256, TK = 64;
     constexpr int UNIT = TM * TK;  // elements of one ring unit: the A or the B half of a k-tile
     constexpr int NU = 5;          // units in the ring
     constexpr int OUTC = (MODE == 0) ? 128 : TN;  // output columns of the block
     constexpr int PITCH = OUTC * 2 + 16;          // bytes per row of the staged output tile
     static_assert(TM == TN && TM * PITCH <= NU * UNIT * 2, "staging tile exceeds LDS");
-    // One array: its address is passed to the copy instructions (inline assembly), which tells
-    // the compiler that all of it may be written there.
-    __shared__ __attribute__((aligned(1024))) char sm_bytes[NU * UNIT * 2];
     bf16_t* const sm = reinterpret_cast<bf16_t*>(sm_bytes);
     if ((int)blockIdx.x >= big_blocks) {  // the remainder blocks after the tiles
         tail_block<MODE>(A, row_token, B, offsets, tail_list, (int)blockIdx.x - big_blocks, d,
@@ -394,8 +393,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
     // would otherwise wait for every copy in flight before each LDS read.  Waits are explicit
     // (ELB_WAIT_VMCNT); M0 carries the LDS destination and is set in the same statement.
     // Each call is 8 copy instructions per wave.
-    // copy instruction i (of 8) of a unit; weights carry the non-temporal hint (streamed, read
-    // by the expert's few M-tiles only)
+    // copy instruction i (of 8) of a unit; nt: the non-temporal hint (the weight copies when
+    // NTW)
     auto issue_one = [&](const bf16_t* src, const uint32_t (&off)[8], int unit, int k0, bool nt,
                          int i) {
         const uint32_t la = lds0 + (uint32_t)unit * (UNIT * 2) + i * 1024;
@@ -478,13 +477,13 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
     // every copy in flight.
     const int nk = Kd / TK;  // >= 1
     // as if barriers at t = -3, -2, -1 had issued B(0); A(0), B(1); A(1), B(2)
-    issue(Bblk, b_off, 0, 0, true);
+    issue(Bblk, b_off, 0, 0, NTW);
     issue(Ablk, a_off, 1, 0, false);
     if (nk > 1) {
-        issue(Bblk, b_off, 2, TK, true);
+        issue(Bblk, b_off, 2, TK, NTW);
         issue(Ablk, a_off, 3, TK, false);
         if (nk > 2) {
-            issue(Bblk, b_off, 4, 2 * TK, true);
+            issue(Bblk, b_off, 4, 2 * TK, NTW);
             ELB_WAIT_VMCNT(24);
         } else {
             ELB_WAIT_VMCNT(16);
@@ -530,7 +529,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
                 if (i < 8) {
                     if (t + 2 < nk) issue_one(Ablk, a_off, ub, (t + 2) * TK, false, i);  // -> unit 2t
                 } else {
-                    if (t + 3 < nk) issue_one(Bblk, b_off, ua, (t + 3) * TK, true, i - 8);
+                    if (t + 3 < nk) issue_one(Bblk, b_off, ua, (t + 3) * TK, NTW, i - 8);
                 }
                 __builtin_amdgcn_sched_barrier(0);
             }
@@ -590,6 +589,23 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
             if (col_ok && r0 + (b + i) * RPI < rows)
                 *reinterpret_cast<u32x4_t*>(dst + (int64_t)(b + i) * RPI * ldc) = v[i];
     }
+}
+
+template <int MODE>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) void gemm_bf16_dma(
+    const bf16_t* __restrict__ A, const int* __restrict__ row_token,
+    const bf16_t* __restrict__ B, const int* __restrict__ offsets,
+    const int* __restrict__ tile_off, const int* __restrict__ tail_list, int big_blocks,
+    int N, int d, int m, bf16_t* __restrict__ C, int nt_weights) {
+    // One array: its address is passed to the copy instructions (inline assembly), which tells
+    // the compiler that all of it may be written there.
+    __shared__ __attribute__((aligned(1024))) char sm_bytes[5 * 256 * 64 * 2];
+    if (nt_weights)  // kernel-uniform
+        gemm_dma_body<MODE, true>(A, row_token, B, offsets, tile_off, tail_list, big_blocks, N,
+                                  d, m, C, sm_bytes);
+    else
+        gemm_dma_body<MODE, false>(A, row_token, B, offsets, tile_off, tail_list, big_blocks, N,
+                                   d, m, C, sm_bytes);
 }
 
 // ------------------------------------------------------------------------------------------
@@ -705,7 +721,7 @@ int gemm_tile_rows(int dtype, int64_t T, int K, int N, int d, int m) {
 hipError_t launch_gemm_gate_up(const void* x, const void* Wgu, const int* row_token,
                                const int* offsets, const int* tile_off, const int* tail_list,
                                int64_t max_tiles, int tile_rows, int d, int N, int m,
-                               int dtype, void* H, hipStream_t s) {
+                               int dtype, void* H, hipStream_t s, bool nt_weights) {
     if (max_tiles <= 0) return hipSuccess;
     if (dtype == ELB_BF16 && tile_rows == LBM) {
         ProfileScope prof("gemm_gate_up_bf16", s);
@@ -713,7 +729,7 @@ hipError_t launch_gemm_gate_up(const void* x, const void* Wgu, const int* row_to
         const unsigned tail = tail_list ? (unsigned)(kTailMax * (m / 32)) : 0u;
         ELB_LAUNCH(gemm_bf16_dma<0>, dim3(big + tail), dim3(256), 0, s,
                            (const bf16_t*)x, row_token, (const bf16_t*)Wgu, offsets, tile_off,
-                           tail_list, (int)big, N, d, m, (bf16_t*)H);
+                           tail_list, (int)big, N, d, m, (bf16_t*)H, (int)nt_weights);
     } else if (dtype == ELB_BF16) {
         ProfileScope prof("gemm_gate_up_bf16_s", s);
         ELB_LAUNCH(gemm_bf16<0>, dim3(grid8(max_tiles * (m / 64))), dim3(256),
@@ -731,7 +747,7 @@ hipError_t launch_gemm_gate_up(const void* x, const void* Wgu, const int* row_to
 hipError_t launch_gemm_down(const void* H, const void* Wd, const int* offsets,
                             const int* tile_off, const int* tail_list, int64_t max_tiles,
                             int tile_rows, int d, int N, int m, int dtype, void* Y,
-                            hipStream_t s) {
+                            hipStream_t s, bool nt_weights) {
     if (max_tiles <= 0) return hipSuccess;
     if (dtype == ELB_BF16 && tile_rows == LBM) {
         ProfileScope prof("gemm_down_bf16", s);
@@ -739,7 +755,7 @@ hipError_t launch_gemm_down(const void* H, const void* Wd, const int* offsets,
         const unsigned tail = tail_list ? (unsigned)(kTailMax * (d / 64)) : 0u;
         ELB_LAUNCH(gemm_bf16_dma<1>, dim3(big + tail), dim3(256), 0, s,
                            (const bf16_t*)H, (const int*)nullptr, (const bf16_t*)Wd, offsets,
-                           tile_off, tail_list, (int)big, N, d, m, (bf16_t*)Y);
+                           tile_off, tail_list, (int)big, N, d, m, (bf16_t*)Y, (int)nt_weights);
     } else if (dtype == ELB_BF16) {
         ProfileScope prof("gemm_down_bf16_s", s);
         ELB_LAUNCH(gemm_bf16<1>, dim3(grid8(max_tiles * ((d + BN - 1) / BN))),
