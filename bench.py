@@ -72,18 +72,18 @@ def time_layer(B, torch, args_gpu, K, mode, steps, warmup, profile, packed=None)
     return e0.elapsed_time(e1) / steps, {n: ms / cnt for n, (ms, cnt) in kern.items()}
 
 
-def settle(B, torch, args_gpu, K, seconds):
-    """Untimed layer calls, elbow and top-K in turn, for about `seconds` of wall time; returns
-    how many were made."""
+def settle(B, torch, args_gpu, K, seconds, topk=True):
+    """Untimed layer calls, elbow and top-K in turn (elbow only without `topk`), for about
+    `seconds` of wall time; returns how many were made."""
     if seconds <= 0:
         return 0
     x, Wr, Wgu, Wd = args_gpu
     calls = [B.elb_moe_forward_prepared(x, Wr, Wgu, Wd, K=K, mode=mode)[0]
-             for mode in (B.MODE_ELBOW, B.MODE_TOPK)]
+             for mode in ((B.MODE_ELBOW, B.MODE_TOPK) if topk else (B.MODE_ELBOW,))]
     n, t0 = 0, time.perf_counter()
     while time.perf_counter() - t0 < seconds:
         for _ in range(10):
-            calls[n % 2]()
+            calls[n % len(calls)]()
             n += 1
         torch.cuda.synchronize()
     return n
@@ -116,15 +116,17 @@ def graph_replay(B, torch, args_gpu, K, mode, steps):
     return e0.elapsed_time(e1) / steps
 
 
-def headline(B, torch, args_gpu, K, steps, warmup, blocks=5):
+def headline(B, torch, args_gpu, K, steps, warmup, blocks=5, topk=True):
     """The headline timing: exactly `steps` elbow-routed layer calls, split into blocks that
     alternate with blocks of the fixed top-K routing on the same inputs (which block of a pair
     goes first alternates too), after `warmup` untimed calls of each.  Each block is bracketed
     by a device synchronisation and timed with events on the stream the library launches on.
-    Returns, per mode, the ms per step over all its blocks and the per-block ms per step."""
+    Without `topk` only the elbow blocks run.  Returns, per mode, the ms per step over all its
+    blocks and the per-block ms per step."""
     x, Wr, Wgu, Wd = args_gpu
+    modes = (B.MODE_ELBOW, B.MODE_TOPK) if topk else (B.MODE_ELBOW,)
     calls = {mode: B.elb_moe_forward_prepared(x, Wr, Wgu, Wd, K=K, mode=mode)[0]
-             for mode in (B.MODE_ELBOW, B.MODE_TOPK)}
+             for mode in modes}
     for _ in range(warmup):
         for c in calls.values():
             c()
@@ -132,9 +134,9 @@ def headline(B, torch, args_gpu, K, steps, warmup, blocks=5):
     nb = max(1, min(blocks, steps))
     sizes = [steps // nb + (1 if i < steps % nb else 0) for i in range(nb)]
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    per = {B.MODE_ELBOW: [], B.MODE_TOPK: []}
+    per = {mode: [] for mode in modes}
     for b, n in enumerate(sizes):
-        order = (B.MODE_ELBOW, B.MODE_TOPK) if b % 2 == 0 else (B.MODE_TOPK, B.MODE_ELBOW)
+        order = modes if b % 2 == 0 else modes[::-1]
         for mode in order:
             torch.cuda.synchronize()
             e0.record()
@@ -145,6 +147,8 @@ def headline(B, torch, args_gpu, K, steps, warmup, blocks=5):
             per[mode].append((e0.elapsed_time(e1), n))
     out = {}
     for name, mode in (("elbow", B.MODE_ELBOW), ("topk", B.MODE_TOPK)):
+        if mode not in per:
+            continue
         tot = sum(ms for ms, _ in per[mode])
         blk = [ms / n for ms, n in per[mode]]
         out[name] = {"ms_per_step": tot / steps, "block_ms_per_step": blk,
@@ -702,6 +706,8 @@ def main():
     ap.add_argument("--routing-counters", action="store_true",
                     help="run only the routing kernel on the routing-only workload (for "
                          "instruction counter runs)")
+    ap.add_argument("--routing-tokens", type=int, default=65536,
+                    help="tokens of the routing-only workload in --routing-counters runs")
     ap.add_argument("--sweep-tokens", default="",
                     help="comma-separated batch sizes: print only the OLMoE-shaped layer's "
                          "timing at each (one JSON line)")
@@ -727,7 +733,7 @@ def main():
         sys.exit(1)
     B.lib()
     if args.routing_counters:
-        routing_only(B, torch, nbuf=4, iters=args.steps)
+        routing_only(B, torch, T=args.routing_tokens, nbuf=4, iters=args.steps)
         return
     if args.sweep_tokens:
         Ts = [int(v) for v in args.sweep_tokens.split(",") if v]
@@ -745,44 +751,50 @@ def main():
     # routing statistics of this batch (for the useful-FLOP count), and the GPU's own logits
     # and routings for the parity counts of the oracle leg
     _, dbg = B.elb_moe_forward(*gpu, K=K, debug=True)
-    _, dbg_top = B.elb_moe_forward(*gpu, K=K, mode=B.MODE_TOPK, debug=True)
+    topk = not args.no_topk
+    dbg_top = B.elb_moe_forward(*gpu, K=K, mode=B.MODE_TOPK, debug=True)[1] if topk else None
     torch.cuda.synchronize()
     ctx = {}
     for name, dd in (("olmoe_prefill_elbow", dbg), ("olmoe_prefill_topk", dbg_top)):
+        if dd is None:
+            continue
         ctx[name] = {"logits": dd["logits"].cpu().numpy(), "k": dd["k"].cpu().numpy(),
                      "ids": dd["ids"].cpu().numpy(), "w": dd["w"].cpu().numpy(), "K": K}
     sum_k = int(dbg["k"].sum().item())
-    sum_k_top = int(dbg_top["k"].sum().item())
+    sum_k_top = int(dbg_top["k"].sum().item()) if topk else None
     counts = dbg["counts"].cpu().numpy()
-    counts_top = dbg_top["counts"].cpu().numpy()
+    counts_top = dbg_top["counts"].cpu().numpy() if topk else None
 
     # A fresh process runs its first few dozen layer calls measurably slower (about 15 %, the
     # clocks and caches settling), so untimed layer calls run for `--settle` seconds before
     # anything is timed.
-    settle_calls = settle(B, torch, gpu, K, args.settle)
+    settle_calls = settle(B, torch, gpu, K, args.settle, topk)
     # headline: exactly --steps elbow layer calls, in blocks alternating with top-K blocks
-    log("headline: %d warmup, %d steps, elbow and top-8 blocks alternating"
-        % (args.warmup, args.steps))
-    hl = headline(B, torch, gpu, K, args.steps, args.warmup)
+    log("headline: %d warmup, %d steps, elbow%s blocks" % (
+        args.warmup, args.steps, " and top-8 alternating" if topk else " only"))
+    hl = headline(B, torch, gpu, K, args.steps, args.warmup, topk=topk)
     ms = hl["elbow"]["ms_per_step"]
-    ms_top = hl["topk"]["ms_per_step"]
+    ms_top = hl["topk"]["ms_per_step"] if topk else None
     # per-kernel durations: the library's per-launch hipEvents over loops of the same calls.
     # Timed launches run slower than untimed back-to-back ones, so the roofline takes the
     # loop that times the two expert GEMMs only (fewer timed launches per layer)
     log("per-kernel timing: %d steps per mode" % args.steps)
     ms_ev, kern = time_layer(B, torch, gpu, K, B.MODE_ELBOW, args.steps, 2, True)
-    ms_ev_top, kern_top = time_layer(B, torch, gpu, K, B.MODE_TOPK, args.steps, 2, True)
     ms_ev_g, kern_g = time_layer(B, torch, gpu, K, B.MODE_ELBOW, args.steps, 2, 2)
-    ms_ev_gt, kern_gt = time_layer(B, torch, gpu, K, B.MODE_TOPK, args.steps, 2, 2)
+    if topk:
+        ms_ev_top, kern_top = time_layer(B, torch, gpu, K, B.MODE_TOPK, args.steps, 2, True)
+        ms_ev_gt, kern_gt = time_layer(B, torch, gpu, K, B.MODE_TOPK, args.steps, 2, 2)
     # per-kernel figures: the expert GEMMs from the loops that time only them, the small
     # kernels from the loops that time every launch (a few us high each)
     kern = {n: kern_g.get(n, v) for n, v in kern.items()}
-    kern_top = {n: kern_gt.get(n, v) for n, v in kern_top.items()}
+    if topk:
+        kern_top = {n: kern_gt.get(n, v) for n, v in kern_top.items()}
     # the same layer call captured in a HIP graph and replayed (launch gaps and host work gone);
     # a supplementary figure: a capture the runtime refuses is reported, not fatal
     try:
         ms_graph = {name: round(graph_replay(B, torch, gpu, K, mode, args.steps), 4)
-                    for name, mode in (("elbow", B.MODE_ELBOW), ("topk", B.MODE_TOPK))}
+                    for name, mode in (("elbow", B.MODE_ELBOW), ("topk", B.MODE_TOPK))
+                    if topk or mode == B.MODE_ELBOW}
     except RuntimeError as exc:
         torch.cuda.synchronize()
         ms_graph = {"error": str(exc)[:200]}
@@ -803,7 +815,7 @@ def main():
             traffic = tj.get("bytes_per_launch")
     flop_all = 6.0 * d * m * sum_k
     kern_sum = sum(kern.values())
-    kern_sum_top = sum(kern_top.values())
+    kern_sum_top = sum(kern_top.values()) if topk else None
     res = {
         "metric": "elbow-routed MoE layer tokens/s (OLMoE shape)",
         "value": round(T / (ms * 1e-3), 1),
@@ -856,10 +868,11 @@ def main():
             "kernel_sum_ms": round(kern_sum_top, 4),
             "ms_per_step_with_kernel_events": round(ms_ev_top, 4),
             "ms_per_step_gemm_timing_loop": round(ms_ev_gt, 4),
-            "kernels_us": {n: round(v * 1e3, 2) for n, v in kern_top.items()}},
-        "elbow_vs_topk_latency_change_pct": round((ms - ms_top) / ms_top * 100, 2),
+            "kernels_us": {n: round(v * 1e3, 2) for n, v in kern_top.items()}} if topk else None,
+        "elbow_vs_topk_latency_change_pct": round((ms - ms_top) / ms_top * 100, 2)
+        if topk else None,
         "elbow_vs_topk_kernel_sum_change_pct": round(
-            (kern_sum - kern_sum_top) / kern_sum_top * 100, 2),
+            (kern_sum - kern_sum_top) / kern_sum_top * 100, 2) if topk else None,
         "paper_context": "the paper reports a 5.3% average latency reduction on OLMoE on one "
                          "NVIDIA H200 (context only)",
     }
@@ -902,8 +915,9 @@ def main():
     }
     res["rows"] = {name: r for name, r in res["rows"].items() if r is not None}
     from paper_2608_04401_amd import stats
-    res["load_balance"] = {k2: (round(v, 5) if isinstance(v, float) else v) for k2, v in
-                           stats.load_balance_report(counts, counts_top, K, T).items()}
+    if topk:
+        res["load_balance"] = {k2: (round(v, 5) if isinstance(v, float) else v) for k2, v in
+                               stats.load_balance_report(counts, counts_top, K, T).items()}
     if not args.no_calibration:
         log("calibration")
         res["calibration"] = calibration(B, torch)
