@@ -13,6 +13,39 @@ namespace elb {
 
 namespace {
 
+// Slots j0 .. j0 + 7 of token t: the row of Y each one adds (-1 past k_t) and its weight.
+// t and K are block-uniform, so these are scalar loads; a whole group of eight is loaded
+// with two 32-byte loads at once (no per-slot branch between dependent loads), and only a
+// group that would run past the token's K slots is loaded slot by slot.
+__device__ __forceinline__ void slot_group(const int* __restrict__ inv,
+                                           const float* __restrict__ w, int64_t t, int K, int j0,
+                                           int kt, int64_t (&r)[8], float (&wj)[8]) {
+    const int64_t base = t * K + j0;
+    int iv[8];
+    float wv[8];
+    if (j0 + 8 <= K) {
+        if (inv) {
+#pragma unroll
+            for (int q = 0; q < 8; ++q) iv[q] = inv[base + q];
+        }
+#pragma unroll
+        for (int q = 0; q < 8; ++q) wv[q] = w[base + q];
+    } else {
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+            const bool in = j0 + q < K;
+            iv[q] = (inv && in) ? inv[base + q] : 0;
+            wv[q] = in ? w[base + q] : 0.f;
+        }
+    }
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+        const bool use = j0 + q < kt;
+        r[q] = use ? (inv ? (int64_t)iv[q] : base + q) : -1;
+        wj[q] = use ? wv[q] : 0.f;
+    }
+}
+
 // NT: the rows are loaded with the non-temporal hint (chosen when Y is larger than the
 // last-level cache, so that it streams from HBM; a smaller Y that the down GEMM has just
 // written is read faster with plain loads)
@@ -39,16 +72,7 @@ __global__ __launch_bounds__(256) void combine_bf16(const bf16_t* __restrict__ Y
         for (int j0 = 0; j0 < kt; j0 += 8) {
             int64_t r[8];
             float wj[8];
-#pragma unroll
-            for (int q = 0; q < 8; ++q) {
-                const int j = j0 + q;
-                r[q] = -1;
-                wj[q] = 0.f;
-                if (j < kt) {
-                    r[q] = inv ? inv[t * K + j] : t * K + j;
-                    wj[q] = w[t * K + j];
-                }
-            }
+            slot_group(inv, w, t, K, j0, kt, r, wj);
             u32x4_t yq[8];
 #pragma unroll
             for (int q = 0; q < 8; ++q) {
@@ -87,16 +111,7 @@ __global__ __launch_bounds__(256) void combine_f32(const float* __restrict__ Y,
         for (int j0 = 0; j0 < kt; j0 += 8) {
             int64_t r[8];
             float wj[8];
-#pragma unroll
-            for (int q = 0; q < 8; ++q) {
-                const int j = j0 + q;
-                r[q] = -1;
-                wj[q] = 0.f;
-                if (j < kt) {
-                    r[q] = inv ? inv[t * K + j] : t * K + j;
-                    wj[q] = w[t * K + j];
-                }
-            }
+            slot_group(inv, w, t, K, j0, kt, r, wj);
             float4 yq[8];
 #pragma unroll
             for (int q = 0; q < 8; ++q)
