@@ -898,6 +898,11 @@ def main():
             "hbm", us_of("router_split_bf16") + us_of("route_split_sum"),
             2 * T * d + 2 * N * d + T * (4 + 8 * K), PEAK_HBM_GBS)
         if us_of("router_split_bf16") > 0 and us_of("route_split_sum") > 0 else None,
+        # the one-launch form (N = 64, d % 256 == 0, T <= 4096): the quarters of the
+        # contraction in one block's waves, then the routing and the dispatch histogram
+        "router + routing (one launch)": row(
+            "hbm", us_of("router_route_dma"), 2 * T * d + 2 * N * d + T * (4 + 8 * K),
+            PEAK_HBM_GBS),
         # the one-kernel form (other bf16 layers with K <= 16): logits kept on chip
         "router + routing fused": row(
             "hbm", us_of("router_route_bf16"), 2 * T * d + 2 * N * d + T * (4 + 8 * K),

@@ -287,6 +287,10 @@ int elb_router_route(const void* x, const void* W_router, int64_t T, int32_t d, 
     if (T == 0) return ELB_OK;
     if (!x || !W_router || !k || !ids || !w)
         return fail(ELB_ERR_INVALID_ARG, "NULL tensor pointer");
+    if (router_route_dma_usable(dtype, T, d, N, params->K))
+        return hip_status(launch_router_route_dma(x, W_router, T, d, *params, logits_out, k,
+                                                  ids, w, nullptr, 0, (hipStream_t)stream),
+                          "router_route");
     return hip_status(launch_router_route(x, W_router, T, d, N, *params, logits_out, k, ids, w,
                                           (hipStream_t)stream),
                       "router_route");
@@ -484,6 +488,15 @@ static int moe_forward_entry(const void* x, const void* W_router, const void* W_
     // routing; the rest the fused one-block kernel, or the router and routing kernels for
     // fp32 and caps above 16.
     const bool skinny = gemm_use_skinny(dtype, T, K, N, d, m);
+    if (router_route_dma_usable(dtype, T, d, N, K)) {
+        if (int rc = hip_status(
+                launch_router_route_dma(x, W_router, T, d, *params, logits_out, k, ids, w,
+                                        (int*)(ws + L.hist), dispatch_hist_ld(T), s),
+                "router_route_dma"))
+            return rc;
+        return experts_impl(x, W_gate_up, W_down, packed, k, ids, w, residual, T, d, N, m, K,
+                            dtype, y, ws, L, counts_out, s, true, split_hist_subs(T));
+    }
     if (router_split_usable(dtype, T, d, N, K) && !skinny) {
         if (int rc = hip_status(
                 launch_router_split_route(x, W_router, T, d, *params, (float*)(ws + L.part),

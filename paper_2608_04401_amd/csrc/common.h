@@ -108,6 +108,17 @@ hipError_t launch_router_route(const void* x, const void* Wr, int64_t T, int d, 
 // into part [4, T, 64] (workspace), then their sum and the routing; also writes the dispatch
 // histogram: split_hist_subs(T) histograms [64, hist_ld] (column g = tokens [64 g, 64 g + 64),
 // or its quarter j in histogram j).  Same bits as the other router paths.
+// router + routing in one launch (N = 64, d % 256 == 0, at most kRouteDmaMaxT tokens,
+// K <= kLaneMaxK): 16 tokens per block, the contraction's quarters in the block's four waves;
+// the same bits as the split form; hist (optional) as launch_router_split_route writes it
+// (kHistSubs histograms, group-major)
+constexpr int64_t kRouteDmaMaxT = 4096;
+static_assert(kRouteDmaMaxT <= 64 * kDirectGroups, "the one-launch form writes kHistSubs "
+                                                   "histograms");
+bool router_route_dma_usable(int dtype, int64_t T, int d, int N, int K);
+hipError_t launch_router_route_dma(const void* x, const void* Wr, int64_t T, int d,
+                                   const elb_route_params& p, float* logits, int* k, int* ids,
+                                   float* w, int* hist, int64_t hist_ld, hipStream_t s);
 bool router_split_usable(int dtype, int64_t T, int d, int N, int K);
 hipError_t launch_router_split_route(const void* x, const void* Wr, int64_t T, int d,
                                      const elb_route_params& p, float* part, float* logits,

@@ -441,6 +441,156 @@ __global__ __launch_bounds__(256) void route_split_sum_x16(const float* __restri
     }
 }
 
+// ---- one launch for router + routing: N = 64, d % 256 == 0, T <= 64 kDirectGroups ----
+//
+// router_route_dma: block b takes tokens [16 b, 16 b + 16) (quarter b % 4 of 64-token group
+// b / 4), wave w quarter w of the contraction (router_slice), as router_split_bf16 does for
+// 64 tokens -- but here the four quarters of a token are in one block, so no partial logits
+// leave the chip and the routing follows in the same launch.  Per 64-column chunk of its
+// quarter a wave copies the 64 W_r rows and the block's 16 x rows (one 128-byte line per row,
+// 16-byte chunks XOR-swizzled by row) straight into its own LDS ring with
+// global_load_lds_dwordx4, kDmaRing - 1 chunks ahead, and waits only for its own copies: the
+// loop has no barrier.  The MFMA chains, the sum ((P0 + P1) + P2) + P3 and the 16-lane routing
+// (route_token_x16) are those of router_split_bf16 + route_split_sum_x16, so the logits,
+// k, ids and weights are the same bits.  hist (optional): the block's per-expert assignment
+// counts go to histogram b % 4, row b / 4, as route_split_sum_x16 writes them (the grid has
+// four blocks per 64-token group; blocks past the last token write zero counts).
+constexpr int kDmaRing = 4;                // chunks in a wave's ring
+constexpr int kDmaSlot = (64 + 16) * 128;  // bytes per chunk: 64 W_r rows, then 16 x rows
+constexpr int kDmaWave = kDmaRing * kDmaSlot;
+
+template <int KMAX>
+__global__ __launch_bounds__(256) void router_route_dma(
+    const bf16_t* __restrict__ x, const bf16_t* __restrict__ Wr, int64_t T, int d, int K,
+    float eps, int mode, int renorm, XTable xt, float* __restrict__ logits,
+    int* __restrict__ kout, int* __restrict__ ids, float* __restrict__ wout,
+    int* __restrict__ hist, int64_t hist_ld) {
+    // the four rings take all of LDS; after the loop a wave's partial tile [16][65] lies at the
+    // start of its own ring, and the 64-bin histogram in wave 1's
+    __shared__ __attribute__((aligned(1024))) char sm[RW * kDmaWave];
+    const int64_t t0 = (int64_t)blockIdx.x * 16;
+    if (t0 >= T) {  // a quarter past the last token of the last group: zero counts only
+        if (hist && threadIdx.x < 64)
+            hist[((int64_t)(blockIdx.x % kHistSubs) * hist_ld + blockIdx.x / kHistSubs) * 64 +
+                 threadIdx.x] = 0;
+        return;  // block-uniform, before any barrier
+    }
+    const int lane = threadIdx.x & 63;
+    const int w = threadIdx.x >> 6;
+    int first, steps;
+    router_slice(d, w, first, steps);  // d % 256 == 0: first and steps are even
+    const int c0 = first / 2, nc = steps / 2;
+    const bf16_t* const xb = x + t0 * d;  // the block's first token row
+    // copy sources: W_r rows 8 i + (lane >> 3) (i < 8) and x rows 8 i + (lane >> 3) (i < 2);
+    // lane l fills physical chunk l & 7 of its row, i.e. it fetches logical chunk
+    // (l & 7) ^ (row & 7).  Rows past T repeat the last token's row (never stored).
+    uint32_t woff[8], xoff[2];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+        const int r = 8 * i + (lane >> 3);
+        const int q = (lane & 7) ^ (r & 7);
+        woff[i] = ((uint32_t)r * (uint32_t)d + c0 * 64 + q * 8) * 2u;
+    }
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+        const int r = 8 * i + (lane >> 3);
+        const int q = (lane & 7) ^ (r & 7);
+        const int tr = (t0 + r < T) ? r : (int)(T - 1 - t0);
+        xoff[i] = ((uint32_t)tr * (uint32_t)d + c0 * 64 + q * 8) * 2u;
+    }
+    char* const ring = sm + w * kDmaWave;
+    const uint32_t lds_ring =
+        __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(lds_void_t*)ring);
+    auto issue = [&](int c, int slot) {  // chunk c of the quarter into ring slot `slot`
+        const uint32_t base = lds_ring + slot * kDmaSlot;
+#pragma unroll
+        for (int i = 0; i < 8; ++i)
+            asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2"
+                         :: "s"(base + i * 1024), "v"(woff[i] + c * 128), "s"(Wr)
+                         : "memory", "m0");
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+            asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2"
+                         :: "s"(base + 64 * 128 + i * 1024), "v"(xoff[i] + c * 128), "s"(xb)
+                         : "memory", "m0");
+    };
+    f32x4_t acc[4];
+#pragma unroll
+    for (int g = 0; g < 4; ++g) acc[g] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    const int l16 = lane & 15, hq = lane >> 4;
+#pragma unroll
+    for (int p = 0; p < kDmaRing - 1; ++p)
+        if (p < nc) issue(p, p);
+    for (int c = 0; c < nc; ++c) {
+        // chunk c is in when at most the copies of the chunks issued after it (at most
+        // kDmaRing - 2 of them, ten instructions each) are in flight; its slot's previous
+        // chunk (c - 1) was read before its MFMAs, so it is free for chunk c + kDmaRing - 1
+        const int left = nc - 1 - c;
+        static_assert(kDmaRing == 4, "wait counts below");
+        if (left >= 2) ELB_WAIT_VMCNT(20);
+        else if (left == 1) ELB_WAIT_VMCNT(10);
+        else ELB_WAIT_VMCNT(0);
+        if (c + kDmaRing - 1 < nc) issue(c + kDmaRing - 1, (c + kDmaRing - 1) % kDmaRing);
+        const char* const sl = ring + (c % kDmaRing) * kDmaSlot;
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {  // the chunk's two 32-deep k-steps
+            const int q = 4 * j + hq;  // logical 16-byte chunk of this lane's 8 k values
+            const bf16x8_t a = *reinterpret_cast<const bf16x8_t*>(
+                sl + 64 * 128 + l16 * 128 + ((q ^ (l16 & 7)) << 4));
+            bf16x8_t b[4];
+#pragma unroll
+            for (int g = 0; g < 4; ++g) {
+                const int n = 16 * g + l16;
+                b[g] = *reinterpret_cast<const bf16x8_t*>(sl + n * 128 + ((q ^ (n & 7)) << 4));
+            }
+#pragma unroll
+            for (int g = 0; g < 4; ++g)
+                acc[g] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b[g], acc[g], 0, 0, 0);
+        }
+    }
+    // this wave's partial tile (lane: tokens 4 hq + r, expert 16 g + l16) at the start of its
+    // own ring: every copy into the ring has landed and every read of it has been used
+    float* const pw = reinterpret_cast<float*>(ring);
+#pragma unroll
+    for (int g = 0; g < 4; ++g)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) pw[(4 * hq + r) * 65 + 16 * g + l16] = acc[g][r];
+    __syncthreads();  // every wave is past its loop and its partial tile is written
+    int* const h = reinterpret_cast<int*>(sm + kDmaWave + 16 * 65 * 4);  // in wave 1's ring
+    if (threadIdx.x < 64) h[threadIdx.x] = 0;
+    // the logits: lane sl of token tr sums elements 4 sl .. 4 sl + 3 of the four partials in
+    // order; the sums replace partial 0 (each word read, then written, by one thread)
+    const int tr = threadIdx.x >> 4, sl = threadIdx.x & 15;
+    const int64_t t = t0 + tr;
+    const bool valid = t < T;
+    float* const row = reinterpret_cast<float*>(sm) + tr * 65;
+    float l4[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int n = 4 * sl + i;
+        const float* p0 = reinterpret_cast<const float*>(sm) + tr * 65 + n;
+        float v = p0[0];
+#pragma unroll
+        for (int ww = 1; ww < RW; ++ww) v += p0[ww * (kDmaWave / 4)];
+        l4[i] = v;
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) row[4 * sl + i] = l4[i];
+    if (logits && valid) {
+        float* const lt = logits + t * 64 + 4 * sl;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) lt[i] = l4[i];
+    }
+    __syncthreads();  // the logit rows and the zeroed histogram before any count
+    route_token_x16<KMAX>(row, K, eps, mode, renorm, xt, t, valid, kout, ids, wout, h);
+    if (!hist) return;  // kernel-uniform
+    __syncthreads();
+    if (threadIdx.x < 64) {
+        const int64_t j = blockIdx.x % kHistSubs, g = blockIdx.x / kHistSubs;
+        hist[(j * hist_ld + g) * 64 + threadIdx.x] = h[threadIdx.x];
+    }
+}
+
 __global__ __launch_bounds__(256) void router_f32(const float* __restrict__ x,
                                                   const float* __restrict__ Wr, int64_t T,
                                                   int d, int N, float* __restrict__ logits) {
@@ -492,6 +642,31 @@ hipError_t launch_router_route(const void* x, const void* Wr, int64_t T, int d, 
     ProfileScope prof("router_route_bf16", s);
     if (p.K <= 8) launch_rr_n<8>(x, Wr, T, d, N, p, logits, k, ids, w, s);
     else launch_rr_n<kLaneMaxK>(x, Wr, T, d, N, p, logits, k, ids, w, s);
+    return hipGetLastError();
+}
+
+bool router_route_dma_usable(int dtype, int64_t T, int d, int N, int K) {
+    // up to one 16-token block per compute unit (256 on MI355X): above that a second round
+    // of blocks costs more than the split form's second launch (measured at 6144 tokens)
+    return dtype == ELB_BF16 && N == 64 && K <= kLaneMaxK && T > 0 && T <= kRouteDmaMaxT &&
+           d % 256 == 0 && d <= (1 << 20);
+}
+
+hipError_t launch_router_route_dma(const void* x, const void* Wr, int64_t T, int d,
+                                   const elb_route_params& p, float* logits, int* k, int* ids,
+                                   float* w, int* hist, int64_t hist_ld, hipStream_t s) {
+    if (T == 0) return hipSuccess;
+    ProfileScope prof("router_route_dma", s);
+    const dim3 grid((unsigned)(dispatch_groups(T) * kHistSubs));  // every histogram quarter
+    const XTable xt = make_xtable(64);
+    if (p.K <= 8)
+        ELB_LAUNCH(router_route_dma<8>, grid, dim3(256), 0, s, (const bf16_t*)x,
+                   (const bf16_t*)Wr, T, d, p.K, p.eps, p.mode, p.renormalize, xt, logits, k,
+                   ids, w, hist, hist_ld);
+    else
+        ELB_LAUNCH(router_route_dma<kLaneMaxK>, grid, dim3(256), 0, s, (const bf16_t*)x,
+                   (const bf16_t*)Wr, T, d, p.K, p.eps, p.mode, p.renormalize, xt, logits, k,
+                   ids, w, hist, hist_ld);
     return hipGetLastError();
 }
 

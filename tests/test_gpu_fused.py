@@ -61,22 +61,28 @@ def test_fused_vs_oracle_olmoe():
                                         (8256, 1024, 12, B.MODE_ELBOW), (3000, 768, 8, B.MODE_ELBOW),
                                         (8192, 512, 8, B.MODE_ELBOW), (8193, 256, 16, B.MODE_TOPK)])
 def test_layer_split_router_equals_fused(T, d, K, mode):
-    """Large batches with N = 64 and d % 256 == 0: the layer computes the router in four blocks
-    per 64 tokens (each a quarter of the contraction) and routes in a second launch, which
-    also writes the dispatch histogram.  Its logits, k, ids and w must be the one-block fused
-    kernel's bits (slices of 1, 2, 3, 4 and 8 64-column chunks; ragged T).  Up to T = 8192 the
-    routing runs 16 tokens per block and writes one histogram per quarter of each 64-token
-    group, which the dispatch adds up; from T = 8193 (and T = 8256) one lane per token with one
-    histogram and the dispatch's scan launch.  Its per-expert counts must be those of its
-    routing, its output the bits of the expert stage run on the same routing (which counts the
-    assignments itself), and the oracle's."""
+    """Batches above 1024 tokens with N = 64 and d % 256 == 0.  Up to T = 4096 the layer (and
+    elb_router_route) take the one-launch router + routing: 16 tokens per block, the four
+    quarters of the contraction in its four waves, then the 16-lane routing and the dispatch
+    histogram of the block's quarter of its 64-token group.  Above 4096 the layer computes the
+    router in four blocks per 64 tokens (each a quarter of the contraction) and routes in a
+    second launch, which also writes the dispatch histogram: up to T = 8192 16 tokens per
+    block, one histogram per quarter of each group, which the dispatch adds up; from T = 8193
+    (and T = 8256) one lane per token with one histogram and the dispatch's scan launch.  The
+    layer's logits, k, ids and w must be the fused entry point's bits and the two-step path's
+    (router kernel, then routing kernel; slices of 1, 2, 3, 4 and 8 64-column chunks; ragged
+    T), its per-expert counts those of its routing, its output the bits of the expert stage
+    run on the same routing (which counts the assignments itself), and the oracle's."""
     L = synth.moe_layer(T, d, 64, 128, dtype="bf16", seed=T + d)
     x, Wr, Wgu, Wd = (to_gpu(a, BF) for a in (L.x, L.W_router, L.W_gu, L.W_down))
     y, dbg = B.elb_moe_forward(x, Wr, Wgu, Wd, K=K, mode=mode, debug=True)
     k, ids, w, lg = B.elb_router_route(x, Wr, K=K, mode=mode, with_logits=True)
+    lg2 = B.elb_router_logits(x, Wr)
+    k2, ids2, w2 = B.elb_route(lg2, K=K, mode=mode)
     torch.cuda.synchronize()
-    assert torch.equal(dbg["logits"], lg)
+    assert torch.equal(dbg["logits"], lg) and torch.equal(lg, lg2)
     assert torch.equal(dbg["k"], k) and torch.equal(dbg["ids"], ids) and torch.equal(dbg["w"], w)
+    assert torch.equal(k, k2) and torch.equal(ids, ids2) and torch.equal(w, w2)
     kk, ii = cpu(k), cpu(ids)
     assert np.array_equal(cpu(dbg["counts"]), np.bincount(ii[ii >= 0], minlength=64))
     assert cpu(dbg["counts"]).sum() == kk.sum()
@@ -91,20 +97,24 @@ def test_layer_split_router_equals_fused(T, d, K, mode):
 
 
 @pytest.mark.parametrize("T,d,K,mode", [(64, 2048, 8, B.MODE_ELBOW), (5, 512, 8, B.MODE_TOPK),
-                                        (1024, 256, 16, B.MODE_ELBOW), (333, 768, 12, B.MODE_ELBOW)])
+                                        (1024, 256, 16, B.MODE_ELBOW), (333, 768, 12, B.MODE_ELBOW),
+                                        (100, 320, 8, B.MODE_ELBOW), (777, 192, 12, B.MODE_TOPK)])
 def test_layer_small_batch_router_equals_fused(T, d, K, mode):
-    """Batches of at most 1024 tokens with N = 64: the layer computes the router as one wave
-    per (16 tokens, 16 experts, quarter of the contraction) and sums the quarters in the
-    16-lane split routing.  Its logits, k, ids and w must be the one-block fused kernel's bits,
-    its per-expert counts those of its routing, and its output the expert stage's bits on the
-    same routing."""
+    """Batches of at most 1024 tokens with N = 64: with d % 256 == 0 the layer takes the
+    one-launch router + routing, otherwise one wave per (16 tokens, 16 experts, quarter of the
+    contraction) and the quarters summed in the 16-lane split routing.  Its logits, k, ids and
+    w must be the fused entry point's bits and the two-step path's, its per-expert counts those
+    of its routing, and its output the expert stage's bits on the same routing."""
     L = synth.moe_layer(T, d, 64, 128, dtype="bf16", seed=T + d + 1)
     x, Wr, Wgu, Wd = (to_gpu(a, BF) for a in (L.x, L.W_router, L.W_gu, L.W_down))
     y, dbg = B.elb_moe_forward(x, Wr, Wgu, Wd, K=K, mode=mode, debug=True)
     k, ids, w, lg = B.elb_router_route(x, Wr, K=K, mode=mode, with_logits=True)
+    lg2 = B.elb_router_logits(x, Wr)
+    k2, ids2, w2 = B.elb_route(lg2, K=K, mode=mode)
     torch.cuda.synchronize()
-    assert torch.equal(dbg["logits"], lg)
+    assert torch.equal(dbg["logits"], lg) and torch.equal(lg, lg2)
     assert torch.equal(dbg["k"], k) and torch.equal(dbg["ids"], ids) and torch.equal(dbg["w"], w)
+    assert torch.equal(k, k2) and torch.equal(ids, ids2) and torch.equal(w, w2)
     kk, ii = cpu(k), cpu(ids)
     assert np.array_equal(cpu(dbg["counts"]), np.bincount(ii[ii >= 0], minlength=64))
     y2 = B.elb_moe_experts(x, Wgu, Wd, k, ids, w)
