@@ -197,10 +197,11 @@ int elb_moe_experts(const void *x, const void *W_gate_up, const void *W_down,
                     void *y, void *workspace, size_t workspace_bytes, void *stream);
 
 /*
- * The whole layer: elb_router_logits, elb_route (fused into elb_router_route for bf16 and
- * K <= 16, except for batches of at most 1024 tokens with N = 64, where the two-step path with
- * its small-batch kernels is faster; both give the same bits), then elb_moe_experts, on one
- * stream, with no host round trip.  Arguments as above; the optional debug outputs (NULL to
+ * The whole layer: elb_router_logits and elb_route (fused as in elb_router_route for bf16 and
+ * K <= 16; with N = 64 the router's contraction is split into four quarters, whose partial
+ * logits are summed in a fixed order before the routing -- one launch up to 4096 tokens when
+ * d % 256 == 0, two above or for other d; every form gives the same bits), then
+ * elb_moe_experts, on one stream, with no host round trip.  Arguments as above; the optional debug outputs (NULL to
  * skip) receive the intermediate results of this call:
  *   logits_out [T, N] float, k_out [T], ids_out [T, K], w_out [T, K],
  *   counts_out [N] int32 (assignments per expert).
