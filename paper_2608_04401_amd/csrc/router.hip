@@ -530,6 +530,8 @@ __global__ __launch_bounds__(256) void router_route_dma(
         if (left >= 2) ELB_WAIT_VMCNT(20);
         else if (left == 1) ELB_WAIT_VMCNT(10);
         else ELB_WAIT_VMCNT(0);
+        // the copies write LDS behind the compiler's back: keep this chunk's reads below the wait
+        asm volatile("" ::: "memory");
         if (c + kDmaRing - 1 < nc) issue(c + kDmaRing - 1, (c + kDmaRing - 1) % kDmaRing);
         const char* const sl = ring + (c % kDmaRing) * kDmaSlot;
 #pragma unroll
