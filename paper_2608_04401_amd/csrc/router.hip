@@ -441,7 +441,7 @@ __global__ __launch_bounds__(256) void route_split_sum_x16(const float* __restri
     }
 }
 
-// ---- one launch for router + routing: N = 64, d % 256 == 0, T <= 64 kDirectGroups ----
+// ---- one launch for router + routing: N = 64, d % 256 == 0, T <= kRouteDmaMaxT ----
 //
 // router_route_dma: block b takes tokens [16 b, 16 b + 16) (quarter b % 4 of 64-token group
 // b / 4), wave w quarter w of the contraction (router_slice), as router_split_bf16 does for
