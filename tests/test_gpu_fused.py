@@ -34,7 +34,8 @@ def _case(T, d, N, K, seed, **kw):
 
 @pytest.mark.parametrize("T,d,N,K", [(4096, 2048, 64, 8), (37, 96, 50, 5), (300, 320, 64, 16),
                                      (5, 544, 3, 2), (64, 2048, 64, 8), (1, 64, 8, 8),
-                                     (1000, 128, 16, 12), (33, 256, 33, 16)])
+                                     (1000, 128, 16, 12), (33, 256, 33, 16), (1, 256, 64, 8),
+                                     (17, 512, 64, 16), (4095, 256, 64, 8)])
 @pytest.mark.parametrize("mode", [B.MODE_ELBOW, B.MODE_TOPK])
 def test_fused_equals_two_step(T, d, N, K, mode):
     _case(T, d, N, K, seed=T + d + N, mode=mode)
@@ -44,6 +45,15 @@ def test_fused_equals_two_step(T, d, N, K, mode):
 @pytest.mark.parametrize("eps", [0.0, 1e-3])
 def test_fused_eps_renorm(eps, renorm):
     _case(1000, 512, 64, 8, seed=3, eps=eps, renormalize=renorm)
+
+
+def test_fused_empty_batch():
+    """T = 0: nothing is launched and the outputs are empty."""
+    x = torch.empty((0, 2048), dtype=BF, device="cuda")
+    Wr = torch.zeros((64, 2048), dtype=BF, device="cuda")
+    k, ids, w, lg = B.elb_router_route(x, Wr, K=8, with_logits=True)
+    torch.cuda.synchronize()
+    assert k.shape == (0,) and ids.shape == (0, 8) and w.shape == (0, 8) and lg.shape == (0, 64)
 
 
 def test_fused_vs_oracle_olmoe():
@@ -98,7 +108,8 @@ def test_layer_split_router_equals_fused(T, d, K, mode):
 
 @pytest.mark.parametrize("T,d,K,mode", [(64, 2048, 8, B.MODE_ELBOW), (5, 512, 8, B.MODE_TOPK),
                                         (1024, 256, 16, B.MODE_ELBOW), (333, 768, 12, B.MODE_ELBOW),
-                                        (100, 320, 8, B.MODE_ELBOW), (777, 192, 12, B.MODE_TOPK)])
+                                        (100, 320, 8, B.MODE_ELBOW), (777, 192, 12, B.MODE_TOPK),
+                                        (1, 256, 8, B.MODE_ELBOW), (65, 1024, 8, B.MODE_TOPK)])
 def test_layer_small_batch_router_equals_fused(T, d, K, mode):
     """Batches of at most 1024 tokens with N = 64: with d % 256 == 0 the layer takes the
     one-launch router + routing, otherwise one wave per (16 tokens, 16 experts, quarter of the
